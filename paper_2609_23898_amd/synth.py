@@ -1,0 +1,290 @@
+"""Seeded synthetic inputs: gradients shaped like the paper's workloads, and
+the random base matrix of the O(eps) plan.
+
+This module is the only code that both the HIP library's callers and the
+oracle's callers use.  It contains none of the method's arithmetic.  It only
+makes numbers.  Every value is a pure function of (seed, stream, index):
+
+* a counter-based splitmix64 hash (Steele, Lea & Flood, "Fast splittable
+  pseudorandom number generators", OOPSLA 2014; the 64-bit finaliser constants
+  as published with splitmix64) gives 64 random bits per counter;
+* an approximately standard normal value is the Irwin-Hall sum of twelve
+  32-bit uniforms minus 6.  It is computed with exact integer arithmetic and
+  one exact scaling by 2^-32, so NumPy, torch on the CPU and torch on the GPU
+  all produce the same bits;
+* a gradient entry is float32(normal * scale), where the scale comes from a
+  per-tensor table computed once on the host.  Every path does the same
+  single float64 product and the same single rounding to float32.
+
+The workloads mirror the paper's experiments: Pythia-1.4B shaped gradients
+(24 layers, d_model 2048, vocabulary 50304, d = 1,414,647,808) and a 12-layer
+GPT-2-small shape (d = 124,439,808) with log-normal per-tensor scales; i.i.d.
+cases; and a heavy-tailed case with 1 % of entries scaled by 100.  They stand
+in for the paper's TinyStories training gradients, which are not used here.
+"""
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+_MASK64 = (1 << 64) - 1
+_GOLDEN = 0x9E3779B97F4A7C15
+_MUL1 = 0xBF58476D1CE4E5B9
+_MUL2 = 0x94D049BB133111EB
+_HASHES_PER_ENTRY = 8            # 6 for the normal, 1 for the outlier mask, 1 spare
+_SCALE_STREAM = 0x5CA1E
+_BASE_STREAM = 0xBA5E
+
+DDP_BUCKET_FLOATS = 25 * 1024 * 1024 // 4    # 25 MiB of fp32, DDP's default cap
+
+
+def _mix64_int(z):
+    """splitmix64 finaliser on a Python int (mod 2^64)."""
+    z &= _MASK64
+    z = ((z ^ (z >> 30)) * _MUL1) & _MASK64
+    z = ((z ^ (z >> 27)) * _MUL2) & _MASK64
+    return z ^ (z >> 31)
+
+
+def stream_key(seed, stream):
+    """64-bit key of one independent stream (e.g. one worker's gradient)."""
+    return _mix64_int(_mix64_int((seed * _GOLDEN + 1) & _MASK64) ^ ((stream * _MUL2) & _MASK64))
+
+
+def _signed(v):
+    v &= _MASK64
+    return v - (1 << 64) if v >= (1 << 63) else v
+
+
+# --- NumPy path (uint64 arithmetic wraps by definition) ---------------------
+
+def _mix64_np(z):
+    z = z ^ (z >> np.uint64(30))
+    z = z * np.uint64(_MUL1)
+    z = z ^ (z >> np.uint64(27))
+    z = z * np.uint64(_MUL2)
+    return z ^ (z >> np.uint64(31))
+
+
+def _hash_np(key, idx, j):
+    ctr = idx.astype(np.uint64) * np.uint64(_HASHES_PER_ENTRY) + np.uint64(j + 1)
+    with np.errstate(over="ignore"):
+        return _mix64_np(np.uint64(key) + ctr * np.uint64(_GOLDEN))
+
+
+def normal_np(key, idx):
+    """Irwin-Hall(12) - 6 at the given counters, float64, exact."""
+    idx = np.asarray(idx, dtype=np.int64)
+    total = np.zeros(idx.shape, dtype=np.int64)
+    with np.errstate(over="ignore"):
+        for j in range(6):
+            h = _hash_np(key, idx, j)
+            total += (h & np.uint64(0xFFFFFFFF)).astype(np.int64)
+            total += (h >> np.uint64(32)).astype(np.int64)
+    return (total + 6 - 6 * (1 << 32)).astype(np.float64) * 2.0 ** -32
+
+
+def uniform32_np(key, idx, j):
+    """One 32-bit uniform integer per counter from hash slot j."""
+    h = _hash_np(key, np.asarray(idx, dtype=np.int64), j)
+    return (h & np.uint64(0xFFFFFFFF)).astype(np.int64)
+
+
+# --- torch path (int64 with explicit logical shifts) -------------------------
+
+def _srl(z, s):
+    return (z >> s) & ((1 << (64 - s)) - 1)
+
+
+def _mix64_torch(z):
+    z = (z ^ _srl(z, 30)) * _signed(_MUL1)
+    z = (z ^ _srl(z, 27)) * _signed(_MUL2)
+    return z ^ _srl(z, 31)
+
+
+def _hash_torch(key, idx, j):
+    ctr = idx * _HASHES_PER_ENTRY + (j + 1)
+    return _mix64_torch(ctr * _signed(_GOLDEN) + _signed(key))
+
+
+def normal_torch(key, idx):
+    """Same values as ``normal_np``; ``idx`` is an int64 torch tensor."""
+    import torch
+    total = torch.zeros_like(idx)
+    for j in range(6):
+        h = _hash_torch(key, idx, j)
+        total += h & 0xFFFFFFFF
+        total += _srl(h, 32)
+    return (total + (6 - 6 * (1 << 32))).to(torch.float64) * 2.0 ** -32
+
+
+def uniform32_torch(key, idx, j):
+    return _hash_torch(key, idx, j) & 0xFFFFFFFF
+
+
+# --- workloads ---------------------------------------------------------------
+
+def gpt2_small_tensor_sizes():
+    """Parameter sizes of a 12-layer GPT-2-small (d_model 768, 50257 tokens,
+    1024 positions, tied output embedding), in parameter order."""
+    d, ff, vocab, ctx = 768, 3072, 50257, 1024
+    sizes = [vocab * d, ctx * d]
+    for _ in range(12):
+        sizes += [d, d,                 # ln_1 weight, bias
+                  d * 3 * d, 3 * d,     # attention c_attn weight, bias
+                  d * d, d,             # attention c_proj weight, bias
+                  d, d,                 # ln_2 weight, bias
+                  d * ff, ff,           # mlp c_fc weight, bias
+                  ff * d, d]            # mlp c_proj weight, bias
+    sizes += [d, d]                     # ln_f weight, bias
+    return sizes
+
+
+def pythia_1_4b_tensor_sizes():
+    """Parameter sizes of Pythia-1.4B (GPT-NeoX, 24 layers, d_model 2048,
+    vocabulary 50304, untied output embedding), in parameter order."""
+    d, ff, vocab = 2048, 8192, 50304
+    sizes = [vocab * d]                 # embed_in
+    for _ in range(24):
+        sizes += [d, d,                 # input_layernorm weight, bias
+                  d, d,                 # post_attention_layernorm weight, bias
+                  3 * d * d, 3 * d,     # query_key_value weight, bias
+                  d * d, d,             # attention dense weight, bias
+                  ff * d, ff,           # dense_h_to_4h weight, bias
+                  d * ff, d]            # dense_4h_to_h weight, bias
+    sizes += [d, d, vocab * d]          # final_layer_norm weight, bias; embed_out
+    return sizes
+
+
+def ddp_buckets(tensor_sizes, cap=DDP_BUCKET_FLOATS):
+    """Greedy DDP-style buckets over the flat gradient: tensors are visited in
+    reverse parameter order; a bucket is closed when the next tensor would push
+    it past ``cap`` floats, and a tensor larger than ``cap`` gets a bucket of its
+    own.  Returns (offset, length) pairs in flat-index order."""
+    offsets = np.concatenate([[0], np.cumsum(tensor_sizes)]).astype(np.int64)
+    buckets = []
+    cur_lo = cur_hi = None
+    for t in reversed(range(len(tensor_sizes))):
+        lo, hi = int(offsets[t]), int(offsets[t + 1])
+        if cur_lo is None:
+            cur_lo, cur_hi = lo, hi
+        elif (cur_hi - lo) > cap:
+            buckets.append((cur_lo, cur_hi - cur_lo))
+            cur_lo, cur_hi = lo, hi
+        else:
+            cur_lo = lo
+    if cur_lo is not None:
+        buckets.append((cur_lo, cur_hi - cur_lo))
+    return sorted(buckets)
+
+
+@dataclass
+class Workload:
+    """One synthetic all-reduce: N workers, c chunks, length-d fp32 gradients.
+
+    ``tensor_sizes`` (optional) splits the flat gradient into tensors, each
+    with its own log-normal scale exp(z_t), z_t ~ N(0,1); otherwise every
+    entry has scale ``scale``.  ``outlier_prob`` entries are multiplied by
+    ``outlier_factor``.
+    """
+    name: str
+    N: int
+    c: int
+    d: int
+    seed: int
+    scale: float = 1.0
+    tensor_sizes: list = None
+    outlier_prob: float = 0.0
+    outlier_factor: float = 1.0
+    buckets: list = None
+    _offsets: np.ndarray = field(default=None, repr=False)
+    _scales: np.ndarray = field(default=None, repr=False)
+
+    def __post_init__(self):
+        if self.tensor_sizes is not None:
+            assert sum(self.tensor_sizes) == self.d, (sum(self.tensor_sizes), self.d)
+            self._offsets = np.concatenate([[0], np.cumsum(self.tensor_sizes)]).astype(np.int64)
+            key = stream_key(self.seed, _SCALE_STREAM)
+            z = normal_np(key, np.arange(len(self.tensor_sizes)))
+            self._scales = np.array([np.float32(math.exp(float(v))) for v in z], dtype=np.float32)
+        else:
+            self._offsets = np.array([0, self.d], dtype=np.int64)
+            self._scales = np.array([np.float32(self.scale)], dtype=np.float32)
+
+    @property
+    def outlier_threshold(self):
+        return int(math.floor(self.outlier_prob * 2.0 ** 32))
+
+    def worker_key(self, worker):
+        return stream_key(self.seed, 1000 + worker)
+
+    def tensor_scales(self):
+        return self._scales.copy()
+
+    def values_np(self, worker, flat_idx):
+        """float32 gradient entries of ``worker`` at flat indices (int array);
+        indices >= d give 0 (the zero pad)."""
+        flat_idx = np.asarray(flat_idx, dtype=np.int64)
+        valid = flat_idx < self.d
+        idx = np.where(valid, flat_idx, 0)
+        key = self.worker_key(worker)
+        n = normal_np(key, idx)
+        if self.outlier_prob > 0:
+            hit = uniform32_np(key, idx, 6) < self.outlier_threshold
+            n = np.where(hit, n * float(self.outlier_factor), n)
+        t = np.searchsorted(self._offsets, idx, side="right") - 1
+        s = self._scales[t].astype(np.float64)
+        v = (n * s).astype(np.float32)
+        return np.where(valid, v, np.float32(0.0))
+
+    def fill_torch(self, out, worker, start=0, chunk=1 << 24):
+        """Write entries [start, start + out.numel()) of ``worker`` into the
+        float32 tensor ``out`` (any device), chunk by chunk."""
+        import torch
+        dev = out.device
+        count = out.numel()
+        key = self.worker_key(worker)
+        offsets = torch.as_tensor(self._offsets, device=dev)
+        scales = torch.as_tensor(self._scales.astype(np.float64), device=dev)
+        flat = out.view(-1)
+        for lo in range(0, count, chunk):
+            hi = min(count, lo + chunk)
+            idx = torch.arange(start + lo, start + hi, dtype=torch.int64, device=dev)
+            valid = idx < self.d
+            idx_c = torch.where(valid, idx, torch.zeros_like(idx))
+            n = normal_torch(key, idx_c)
+            if self.outlier_prob > 0:
+                hit = uniform32_torch(key, idx_c, 6) < self.outlier_threshold
+                n = torch.where(hit, n * float(self.outlier_factor), n)
+            t = torch.searchsorted(offsets, idx_c, right=True) - 1
+            v = (n * scales[t]).to(torch.float32)
+            flat[lo:hi] = torch.where(valid, v, torch.zeros_like(v))
+        return out
+
+
+def base_matrix(seed, N, c):
+    """N x c base matrix B with i.i.d. approximately N(0,1) entries (the paper's
+    choice of B for the O(eps) plan, appendix on the experiments), float64."""
+    return normal_np(stream_key(seed, _BASE_STREAM), np.arange(N * c)).reshape(N, c)
+
+
+def workload(cfg):
+    """The five synthetic workloads, by number (1..5)."""
+    if cfg == 1:
+        return Workload("tiny N=4 c=4 d=4096 iid N(0,1)", 4, 4, 4096, seed=1)
+    if cfg == 2:
+        return Workload("N=8 c=16 d=2^24 iid N(0,1e-6)", 8, 16, 1 << 24, seed=2, scale=1e-3)
+    if cfg == 3:
+        sizes = gpt2_small_tensor_sizes()
+        return Workload("GPT-2-small N=8 c=32 d=124439808 lognormal tensors, 25MiB buckets",
+                        8, 32, sum(sizes), seed=3, tensor_sizes=sizes,
+                        buckets=ddp_buckets(sizes))
+    if cfg == 4:
+        sizes = pythia_1_4b_tensor_sizes()
+        return Workload("Pythia-1.4B N=8 c=64 d=1414647808 lognormal tensors",
+                        8, 64, sum(sizes), seed=4, tensor_sizes=sizes)
+    if cfg == 5:
+        return Workload("N=16 c=128 d=4e8 iid N(0,1), 1% x100 outliers", 16, 128,
+                        400_000_000, seed=5, outlier_prob=0.01, outlier_factor=100.0)
+    raise ValueError(cfg)
