@@ -1,0 +1,277 @@
+#!/usr/bin/env python3
+"""Throughput of the CERAR hot path on one MI355X.
+
+One step = the whole approximate all-reduce for all N simulated workers:
+encode (K1), rounds 1..L (K2/K3; round L only relabels) and decode (K4), on
+synthetic gradients already resident in HBM.  The metric is the algorithmic
+HBM traffic of the step, N * (8c + 3N - 9) * p * 4 bytes, divided by the
+step time, in GB/s; its share of the 8 TB/s HBM peak is reported beside it.
+
+Default workload: N = 8 workers, c = 64 chunks, d = 1,414,647,808 fp32
+(Pythia-1.4B-shaped gradients with log-normal per-tensor scales), plan from
+the condition-number-constrained design with kappa_max = 1e3.
+
+The timed steps call the per-step entry points (the same launches
+cerar_ring_simulate makes) with HIP events between the phases on the launch
+stream; those events give each kernel's average duration.  A second timed
+loop of single cerar_ring_simulate calls cross-checks the step time.  The fp64
+CPU oracle is timed on a bounded sample of positions (cpu_baseline).
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "encode+round+decode GB/s per worker (% HBM peak), N=8 c=64 d=1.4e9 fp32"
+HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = headline)")
+    ap.add_argument("--plan-iters", type=int, default=100, help="ALS iterations of the kappa design")
+    ap.add_argument("--cpu-positions", type=int, default=1 << 19,
+                    help="positions of the bounded oracle sample (0 = skip cpu_baseline)")
+    ap.add_argument("--copy-floats", type=int, default=1 << 30, help="size of the copy reference")
+    return ap.parse_args()
+
+
+def product_plan(C, wl, iters):
+    if wl.N == 4 and wl.c == 4:
+        return C.Plan(wl.N, wl.c, "vandermonde", 0.5), "Vandermonde tau=0.5 (Chebyshev nodes)"
+    if wl.c == 16:
+        return C.Plan(wl.N, wl.c, "o_eps", 1e-3, seed=1000 + wl.N), "O(eps) eps=1e-3"
+    if wl.c == 128:
+        return C.Plan(wl.N, wl.c, "o_eps", 1e-2, seed=1000 + wl.N), "O(eps) eps=1e-2"
+    return (C.Plan(wl.N, wl.c, "kappa", 1e3, seed=1000 + wl.N, eps0=0.3, als_iters=iters),
+            f"kappa_max=1e3 ALS {iters} it from O(0.3)")
+
+
+def family_of(k, N, c, L):
+    if k <= N - 1:
+        return "k_round<0> (K2: recv + delta)"
+    if k < L:
+        return "k_round<1> (K3: recv - delta + delta)" if k + 1 <= c else "k_round<2> (K3: recv - delta)"
+    return None
+
+
+def cpu_baseline(wl, S):
+    """Time the fp64 oracle (its own plan) on S sampled positions of the
+    same workload, on one host thread."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_limits
+
+    from oracle import plan as OP
+    from oracle import ring as OR
+    from paper_2609_23898_amd import synth
+
+    N, c, d = wl.N, wl.c, wl.d
+    p = -(-d // c)
+    rng = np.random.default_rng(12345)
+    pos = np.unique(np.concatenate([rng.integers(0, p, size=S - 1), [p - 1]]))
+    S = pos.size
+    flat = (np.arange(c)[None, :] * p + pos[:, None]).astype(np.int64)       # S x c
+    # the shared generator gives the same bits on any device; run it on the GPU
+    idx = torch.from_numpy(flat.ravel()).to("cuda:0")
+    G = [wl.values_torch(w, idx).cpu().numpy().reshape(S, c).astype(np.float64) for w in range(N)]
+    del idx
+    with threadpool_limits(limits=1):
+        if wl.c == 64 or wl.c == 32:
+            B = synth.base_matrix(1000 + N, N, c)
+            U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(c)), 0.3, 1e3, 20)
+            plan_desc = "oracle kappa design (20 ALS iterations)"
+        else:
+            B = synth.base_matrix(1000 + N, N, c)
+            U, R = OP.mpc_plan(B, OP.o_eps_perturbation(np.diag(OP.chebyshev_nodes(c)), 0.3))
+            plan_desc = "oracle O(eps) plan"
+        t0 = time.perf_counter()
+        out = OR.allreduce_chunks(G, U, R)
+        dt = time.perf_counter() - t0
+    assert all(np.all(np.isfinite(o)) for o in out)
+    bytes_sample = N * (8 * c + 3 * N - 9) * S * 4
+    return {"value": bytes_sample / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "seconds": dt,
+            "sample": f"{S} positions x {c} chunks x {N} workers of the same workload "
+                      f"({S / p:.2e} of the positions), fp64 NumPy oracle "
+                      f"(encode, Algorithm 1 lock-step, decode) with its {plan_desc}; "
+                      f"GB/s counts the same algorithmic bytes per position as the GPU line"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs the single-GPU simulation of all N workers; --gpus {args.gpus} is not "
+              "supported (multi-GPU CERAR is not part of this build)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2609_23898_amd import cerar as C
+    from paper_2609_23898_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    wl = synth.workload(args.config)
+    N, c, d = wl.N, wl.c, wl.d
+    t = time.perf_counter()
+    plan, plan_desc = product_plan(C, wl, args.plan_iters)
+    info = plan.info()
+    log(f"plan: {plan_desc} kappa_M={info['kappa_M']:.3g} phi={info['phi']:.4g} "
+        f"({time.perf_counter() - t:.1f}s)")
+    L = plan.L
+    p, _ = plan.chunk_len(d)
+
+    t = time.perf_counter()
+    grads = torch.empty((N, d), dtype=torch.float32, device=dev)
+    for w in range(N):
+        wl.fill_torch(grads[w], w)
+    work, ws, out = C.allocate(plan, d, dev)
+    torch.cuda.synchronize()
+    log(f"inputs: N={N} c={c} d={d} p={p} L={L} generated in {time.perf_counter() - t:.1f}s; "
+        f"{(grads.numel() + work.numel() + out.numel()) * 4 / 1e9 + ws.numel() / 1e9:.1f} GB resident")
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        C.encode_round(plan, 0, d, grads, work, ws)
+        if ev is not None:
+            ev[1].record()
+        for k in range(1, L + 1):
+            C.encode_round(plan, k, d, grads, work, ws)
+            if ev is not None:
+                ev[k + 1].record()
+        C.decode(plan, d, work, ws, out)
+        if ev is not None:
+            ev[L + 2].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(L + 3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(events[s])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+
+    # cross-check: the single-call entry point
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        C.ring_simulate(plan, d, grads, work, ws, out)
+    torch.cuda.synchronize()
+    ms_ring = (time.perf_counter() - t2) * 1e3 / args.steps
+
+    # per-kernel durations from the events
+    fam_time, fam_count, fam_bytes = {}, {}, {}
+    bw = C.phase_bytes_per_worker(N, c, p)
+    flops = C.phase_flops_per_worker(N, c, p)
+
+    def add(name, ms, nbytes):
+        fam_time[name] = fam_time.get(name, 0.0) + ms
+        fam_count[name] = fam_count.get(name, 0) + 1
+        fam_bytes[name] = nbytes
+
+    for ev in events:
+        add("k_encode (K1)", ev[0].elapsed_time(ev[1]), N * bw["encode"])
+        for k in range(1, L + 1):
+            fam = family_of(k, N, c, L)
+            if fam:
+                add(fam, ev[k].elapsed_time(ev[k + 1]), N * bw["rounds"][k])
+        add("k_decode (K4)", ev[L + 1].elapsed_time(ev[L + 2]), N * bw["decode"])
+    kernels = {}
+    for name in fam_time:
+        avg = fam_time[name] / fam_count[name]
+        kernels[name] = {"launches_per_step": fam_count[name] // args.steps,
+                         "avg_ms": avg, "ms_per_step": fam_time[name] / args.steps,
+                         "bytes_per_launch": fam_bytes[name],
+                         "gbps": fam_bytes[name] / (avg * 1e-3) / 1e9}
+    for name, key in (("k_encode (K1)", "encode"), ("k_decode (K4)", "decode")):
+        kernels[name]["tflops"] = N * flops[key] / (kernels[name]["avg_ms"] * 1e-3) / 1e12
+        kernels[name]["mfma_frac"] = kernels[name]["tflops"] / FP32_MFMA_PEAK_TFLOPS
+    dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
+    dk = kernels[dominant]
+
+    # achievable-bandwidth reference: a plain copy kernel
+    nf = min(args.copy_floats, grads.numel())
+    src = grads.view(-1)[:nf]
+    dst = out.view(-1)[:nf]
+    for _ in range(2):
+        C.copy_f32(dst, src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        C.copy_f32(dst, src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 2 * nf * 4 * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+    # approximation error of the decoded sums (K5, not timed)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    norms = torch.empty(N + 1, dtype=torch.float64, device=dev)
+    C.error_norms(N, d, grads, out, norms)
+    nm = norms.cpu().numpy()
+    rel_err = [math.sqrt(nm[i] / nm[N]) for i in range(N)]
+
+    step_bytes = N * C.algorithmic_bytes_per_worker(N, c, p)
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "N": N, "c": c, "d": d, "p": p, "L": L,
+                   "plan": plan_desc, "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+                   "bytes_per_step": step_bytes, "encode": "out of place (grads kept for every step)"},
+        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
+                     "traffic": None},
+        "kernels": kernels,
+        "ms_per_step_ring_simulate": round(ms_ring, 4),
+        "copy_gbps": round(copy_gbps, 1),
+        "approx_rel_err_max": max(rel_err),
+        "plan_info": {k: info[k] for k in ("kappa_M", "kappa_U", "kappa_R", "phi", "phi_closed_form",
+                                            "comm_rate", "storage_rate", "r_star", "fp64_reliable")},
+    }
+    del grads, work, ws, out
+    torch.cuda.empty_cache()
+    if args.cpu_positions > 0:
+        t = time.perf_counter()
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_positions)
+        log(f"cpu baseline: {result['cpu_baseline']['value']:.3f} GB/s ({time.perf_counter() - t:.1f}s total)")
+    for k, v in list(result["plan_info"].items()):
+        if isinstance(v, float) and not math.isfinite(v):
+            result["plan_info"][k] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

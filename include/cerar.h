@@ -1,0 +1,216 @@
+/*
+ * cerar.h - C ABI of libcerar, an MI355X (gfx950) implementation of the
+ * data-parallel hot path of CERAR, the communication-efficient approximate
+ * ring all-reduce of Munim & Ramamoorthy ("Communication-Efficient
+ * Distributed Training via Ring-Based Coded Approximate All-Reduce").
+ *
+ * The method (Sec. II): each of N workers splits its length-d gradient into
+ * c chunks of p = ceil(d/c) floats (zero pad), encodes them linearly
+ * (Delta_i = G_i U_i), runs L = c + N - 2 combine-and-forward rounds on a ring
+ * (Algorithm 1, update equations (2)), and decodes its L+1 stored
+ * observations linearly (g_hat_i = Y_i R_i) into an approximation of the sum
+ * of all N gradients.
+ *
+ * On one GPU all N workers live in one HBM allocation: worker i's buffers
+ * are slices of caller-owned arrays, and a send is a handoff of a p-float
+ * slot from W_i to W_{i+1}: no bytes move, only the ownership table changes.
+ *
+ * Conventions for every call
+ *  - Return value: a cerar_status.  Details of the last non-OK status of the
+ *    calling thread are in cerar_last_error().
+ *  - Pointers named "device" are HIP device memory of the current device,
+ *    owned by the caller; the library never frees caller memory.
+ *  - Calls taking a stream only validate and enqueue work on that stream
+ *    (NULL = the legacy default stream); they never synchronise.  Work
+ *    enqueued by calls that share buffers must be ordered by the caller
+ *    (one stream does that).
+ *  - All floating point on the device is IEEE fp32; plan construction is
+ *    host fp64.
+ */
+#ifndef CERAR_H
+#define CERAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t. */
+typedef struct ihipStream_t *cerar_stream;
+
+typedef enum {
+    CERAR_OK = 0,
+    CERAR_E_INVAL = -1,    /* an argument is out of range or NULL */
+    CERAR_E_NOMEM = -2,    /* host or device allocation failed */
+    CERAR_E_SINGULAR = -3, /* some window A_l of the construction is exactly singular */
+    CERAR_E_NOCONV = -4,   /* an iterative host routine did not converge */
+    CERAR_E_DEVICE = -5,   /* a HIP call failed; the HIP error text is in cerar_last_error() */
+    CERAR_E_STATE = -6     /* cerar_encode_round / cerar_decode called out of order */
+} cerar_status;
+
+typedef enum {
+    CERAR_VANDERMONDE = 0, /* Sec. II-B: z_j = exp(tau xi_j), b_l = [z_j^l], D = diag(z_j^N); param = tau > 0 */
+    CERAR_O_EPS = 1,       /* Sec. II-C: B ~ N(0,1), D = I + eps H; param = eps >= 0 with eps ||H||_2 < 1 */
+    CERAR_KAPPA = 2,       /* Sec. II-D, eq. (16): ALS under kappa_2(M_i) <= param = kappa_max >= sqrt(N) */
+    CERAR_EXPLICIT = 3     /* caller-supplied U and R (cerar_plan_create_explicit) */
+} cerar_construction;
+
+/* Opaque plan: N, c, the fp64 matrices (U_k)_{k<N}, (R_i)_{i<N}, their fp32
+ * device copies in the kernels' operand layout, and the slot-ownership
+ * tables of the handoff ring.  Immutable after creation; may be shared by
+ * threads. */
+typedef struct cerar_plan cerar_plan;
+
+/* Full description for cerar_plan_create_desc.  Zero-initialise, then set
+ * N, c, kind and param; every other field has a default. */
+typedef struct {
+    int N;                  /* workers, 2 <= N <= 64 */
+    int c;                  /* chunks, N <= c <= 128 (c = N is the exact ring all-reduce) */
+    cerar_construction kind;
+    double param;           /* tau (VANDERMONDE), eps (O_EPS), kappa_max (KAPPA) */
+    uint64_t seed;          /* seeds B when base == NULL (splitmix64 + Box-Muller) */
+    const double *base;     /* optional host N x c row-major B (O_EPS, KAPPA) */
+    const double *perturb;  /* optional host c x c row-major H (O_EPS, KAPPA); default diag(nodes) */
+    const double *nodes;    /* optional host c distinct reals xi; default cos((2j-1) pi / 2c) */
+    double eps0;            /* KAPPA: eps of the O(eps) starting plan; <= 0 selects 0.3 */
+    int als_iters;          /* KAPPA: ALS iterations (U-step, R-step, projection); <= 0 selects 100 */
+} cerar_plan_desc;
+
+/* Plan diagnostics (host fp64). */
+typedef struct {
+    int N, c, L, r_star;          /* L = c+N-2 (Sec. II); r_star = ceil(c/N)-1 (Sec. II-C) */
+    cerar_construction kind;
+    double param;
+    double phi;                   /* Phi(U,R) = sum_i ||M_i R_i - T||_F^2, eq. (7) */
+    double phi_closed_form;       /* N(N-1)/2 ||D^-1 - I||_F^2 (Prop. 2) for MPC plans, else NaN */
+    double phi_initial;           /* KAPPA: Phi of the O(eps0) starting plan, else NaN */
+    double kappa_M;               /* max_i kappa_2(M_i), the constrained quantity of eq. (16) */
+    double kappa_U;               /* max_k kappa_2(U_k) */
+    double kappa_R;               /* max_i kappa_2(R_i) */
+    double amplification;         /* max_k ||U_k||_2 * max_i ||R_i||_2 */
+    double comm_rate;             /* L/c = 1 + (N-2)/c (Sec. II-B) */
+    double storage_rate;          /* 1 + N/c (Sec. II-B) */
+    double proj_a0, proj_b0;      /* KAPPA: last projection interval, else NaN */
+    int fp64_reliable;            /* 0 when kappa_U * c * 2^-53 > 1e-6: fp64 inverses lose digits */
+    uint64_t seed_used;           /* seed that produced B (after retries), 0 if B was given */
+} cerar_plan_info;
+
+/* Build a plan on the host in fp64 (Sec. II-B to II-D): B and D (or the
+ * nodes) of the chosen construction, then U_k = A_{N-1-k}^{-1} (eq. (10)) and
+ * R_i[l,:] = a_{l-i} (eq. (11)); KAPPA then runs the alternating least squares
+ * of Sec. II-D from the O(eps0) plan.  Synchronous; touches no device.
+ * Errors: E_INVAL (N < 2, N > 64, c < N, c > 128, param out of range,
+ * out == NULL), E_SINGULAR (a window A_l exactly singular for 8 seeds, or for
+ * the given B), E_NOMEM. */
+int cerar_plan_create(int N, int c, cerar_construction kind, double param,
+                      uint64_t seed, cerar_plan **out);
+int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **out);
+
+/* Plan from caller matrices: U is host [N][c][c] with U[k][l][j] the
+ * coefficient of chunk l in delta_{k,j+1}; R is host [N][L+1][c] with R[i][k][m]
+ * the weight of y_{i,k+1} in output chunk m.  Copied. */
+int cerar_plan_create_explicit(int N, int c, const double *U, const double *R,
+                               cerar_plan **out);
+
+/* Frees host and device memory of the plan.  No work using it may be pending. */
+void cerar_plan_destroy(cerar_plan *plan);
+
+int cerar_plan_get_info(const cerar_plan *plan, cerar_plan_info *info);
+
+/* Copies the fp64 matrices into host arrays laid out as in
+ * cerar_plan_create_explicit (N*c*c and N*(L+1)*c doubles). Either may be NULL. */
+int cerar_plan_get_matrices(const cerar_plan *plan, double *U, double *R);
+
+/* Geometry for gradient length d: p = ceil(d/c) (message length, Sec. II)
+ * and the stride of pool slots in the workspace (p rounded up to 64). */
+int cerar_chunk_len(const cerar_plan *plan, size_t d, size_t *p, size_t *pool_stride);
+
+/* Device workspace needed for gradient length d: the pool of N*N message
+ * slots that the first N sends of every worker need (the other c slots of
+ * each worker are its own encoded chunks, overwritten in place). */
+int cerar_workspace_bytes(const cerar_plan *plan, size_t d, size_t *bytes);
+
+/* Ownership table after step `step` (0 = encode, k = round 1..L): writes
+ * N*(c+N) ints, per worker i: the slots of D_{i,1..c} (c), of B_{i,1..N-1}
+ * (N-1), and of the next message x_{i,step+1} (1; -1 after round L-1).
+ * Slot s < N*c is chunk (s % c) of worker (s / c) in `work`; slot s >= N*c
+ * is pool slot (s - N*c) of the workspace. */
+int cerar_slot_map(const cerar_plan *plan, int step, int *slots);
+
+/* One step of the protocol for all N workers on `stream`.
+ *  step 0   encode (Sec. II, "Initialization"): for every worker i and
+ *           position e < p, delta_{i,j}[e] = sum_l U_i[l][j-1] g_i[l p + e]
+ *           (entries at l p + e >= d read as the zero pad), written to
+ *           work[i*ld_work + (j-1)*p + e]; the first send x_{i,1} = delta_{i,1}
+ *           is also written to worker i's first pool slot.
+ *  step k   round k of Algorithm 1 / eq. (2), 1 <= k <= L: W_i takes the
+ *           slot holding x_{i-1,k}; rounds k <= N-1 keep it as B_{i,k} and
+ *           form x_{i,k+1} = x_{i-1,k} + delta_{i,k+1} in a fresh pool slot;
+ *           rounds k >= N keep it as D_{i,j} (j = k-N+1) and, if k < L, form
+ *           x_{i,k+1} = (x_{i-1,k} - delta_{i,j}) [+ delta_{i,k+1} if k < c]
+ *           in the slot that held delta_{i,j}.  Round L only relabels.
+ * grads:  device, N slices of >= d floats at stride ld_grads (read at step 0 only).
+ * work:   device, N slices of >= c*p floats at stride ld_work; may equal
+ *         grads (in-place encode, the paper's storage discipline) when
+ *         ld_work == ld_grads.
+ * ws:     device, cerar_workspace_bytes(plan, d).
+ * Steps must run in order 0, 1, .., L on the same (work, ws): the library
+ * keeps the next expected step per workspace address and returns E_STATE
+ * otherwise (step 0 is always accepted and restarts the sequence). */
+int cerar_encode_round(const cerar_plan *plan, int step, size_t d,
+                       const float *grads, size_t ld_grads,
+                       float *work, size_t ld_work, void *ws, cerar_stream stream);
+
+/* Decode (Sec. II-A): g_hat_i = Y_i R_i with Y_i = [B_{i,1..N-1} | D_{i,1..c}]
+ * read from the slots the ownership table names after round L.  Writes the
+ * first d floats of out[i*ld_out ..] for every worker; nothing beyond d.
+ * out must not overlap work or ws.  E_STATE unless rounds 1..L completed
+ * on this workspace. */
+int cerar_decode(const cerar_plan *plan, size_t d, const float *work, size_t ld_work,
+                 const void *ws, float *out, size_t ld_out, cerar_stream stream);
+
+/* Encode, L rounds and decode for all N workers: the whole approximate
+ * all-reduce, enqueued on `stream` (L + 1 kernel launches: round L has none). */
+int cerar_ring_simulate(const cerar_plan *plan, size_t d,
+                        const float *grads, size_t ld_grads,
+                        float *work, size_t ld_work, void *ws,
+                        float *out, size_t ld_out, cerar_stream stream);
+
+/* Bucketed all-reduce (one independent CERAR instance per bucket, the same
+ * plan for all): bucket b covers flat entries [bucket_off[b],
+ * bucket_off[b] + bucket_len[b]) of every worker's gradient and gets its own
+ * p_b = ceil(bucket_len[b]/c).  work holds, per worker, the buckets' c*p_b
+ * slots back to back (stride ld_work >= sum_b c*p_b); ws is
+ * cerar_bucketed_workspace_bytes.  Every round is one launch for all
+ * buckets and workers.  bucket_off/bucket_len are host arrays. */
+int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len,
+                                   int nbuckets, size_t *work_floats, size_t *ws_bytes);
+int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,
+                                 const size_t *bucket_off, const size_t *bucket_len,
+                                 const float *grads, size_t ld_grads,
+                                 float *work, size_t ld_work, void *ws,
+                                 float *out, size_t ld_out, cerar_stream stream);
+
+/* Error norms (the metric of Table 3, relative l2 error per worker):
+ * norms (device, N+1 doubles) receives sum_e (out_i[e] - S[e])^2 for
+ * i = 0..N-1, then sum_e S[e]^2, where S = sum_w grads_w (fp64) over
+ * e < d.  Overwrites norms. */
+int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_grads,
+                      const float *out, size_t ld_out, double *norms,
+                      cerar_stream stream);
+
+/* Measurement helper: dst[0..n) = src[0..n), a plain streaming copy used as
+ * the achievable-bandwidth reference and as the known-size kernel that
+ * scales the HBM traffic counters. */
+int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stream stream);
+
+/* Text of the calling thread's last non-OK status ("" if none). */
+const char *cerar_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CERAR_H */

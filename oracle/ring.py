@@ -52,7 +52,8 @@ def run_protocol(Delta, trace=None):
     to receiver.  Returns (Y, stats): Y[i] is the p x (L+1) matrix
     [B_{i,1} .. B_{i,N-1} | D_{i,1} .. D_{i,c}] and stats counts rounds and the
     floats each worker sent.  If ``trace`` is a list, one dict per round is
-    appended with the transmitted x_{i,k} and the rolling states sigma_{i,k}.
+    appended with the transmitted x_{i,k}, the rolling states sigma_{i,k} and
+    copies of the D and B buffers after the round.
     """
     N = len(Delta)
     p, c = np.asarray(Delta[0]).shape
@@ -83,7 +84,10 @@ def run_protocol(Delta, trace=None):
         if trace is not None:
             trace.append({"k": k,
                           "x": [s.copy() for s in sent],
-                          "sigma": [ci.copy() for ci in C]})
+                          "sigma": [ci.copy() for ci in C],
+                          "D": [[v.copy() for v in D[i]] for i in range(N)],
+                          "B": [[None if v is None else v.copy() for v in Bstore[i]]
+                                for i in range(N)]})
     Y = [np.column_stack(Bstore[i] + D[i]) for i in range(N)]
     stats = {"rounds": L, "message_len": p, "sent_floats": sent_floats,
              "slots_per_worker": c + (N - 1) + 1}

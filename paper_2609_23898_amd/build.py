@@ -1,0 +1,55 @@
+"""Compiles libcerar.so in-tree with hipcc for gfx950."""
+
+import os
+import shutil
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+OUT = os.path.join(HERE, "libcerar.so")
+
+HIP_SOURCES = ["kernels.hip"]
+CXX_SOURCES = ["plan.cpp", "linalg.cpp"]
+
+# Packed fp32 instructions stay disabled in every HIP translation unit.
+HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-Wall", "-Wno-unused-result"]
+CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
+
+
+def _run(cmd):
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError("command failed: " + " ".join(cmd))
+    return r
+
+
+def build(verbose=False):
+    hipcc = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    tmp = os.path.join(HERE, "_build")
+    os.makedirs(tmp, exist_ok=True)
+    objs = []
+    for src in CXX_SOURCES:
+        obj = os.path.join(tmp, src + ".o")
+        _run(["g++", *CXX_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
+              os.path.join(CSRC, src), "-o", obj])
+        objs.append(obj)
+    for src in HIP_SOURCES:
+        obj = os.path.join(tmp, src + ".o")
+        _run([hipcc, *HIP_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
+              os.path.join(CSRC, src), "-o", obj])
+        objs.append(obj)
+    tmp_out = OUT + ".tmp"
+    _run([hipcc, "-shared", "--offload-arch=gfx950", "-fPIC", *objs, "-o", tmp_out, "-lpthread"])
+    os.replace(tmp_out, OUT)
+    if verbose:
+        print("built", OUT)
+    return OUT
+
+
+if __name__ == "__main__":
+    build(verbose=True)

@@ -1,0 +1,303 @@
+"""Python binding of libcerar (ctypes).  Argument marshalling only: every
+step of the all-reduce runs in the library's HIP kernels; torch supplies
+device memory and the stream.
+
+The in-tree ``libcerar.so`` is required: importing this module raises if it
+has not been built (``__graft_entry__.build()``), and there is no fallback.
+"""
+
+import ctypes
+import math
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcerar.so")
+
+VANDERMONDE, O_EPS, KAPPA, EXPLICIT = 0, 1, 2, 3
+_KINDS = {"vandermonde": VANDERMONDE, "o_eps": O_EPS, "kappa": KAPPA, "explicit": EXPLICIT}
+
+STATUS = {0: "OK", -1: "E_INVAL", -2: "E_NOMEM", -3: "E_SINGULAR", -4: "E_NOCONV",
+          -5: "E_DEVICE", -6: "E_STATE"}
+
+
+class CerarError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+class PlanDesc(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int), ("c", ctypes.c_int), ("kind", ctypes.c_int),
+                ("param", ctypes.c_double), ("seed", ctypes.c_uint64),
+                ("base", ctypes.POINTER(ctypes.c_double)),
+                ("perturb", ctypes.POINTER(ctypes.c_double)),
+                ("nodes", ctypes.POINTER(ctypes.c_double)),
+                ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int)]
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int), ("c", ctypes.c_int), ("L", ctypes.c_int), ("r_star", ctypes.c_int),
+                ("kind", ctypes.c_int), ("param", ctypes.c_double),
+                ("phi", ctypes.c_double), ("phi_closed_form", ctypes.c_double),
+                ("phi_initial", ctypes.c_double), ("kappa_M", ctypes.c_double),
+                ("kappa_U", ctypes.c_double), ("kappa_R", ctypes.c_double),
+                ("amplification", ctypes.c_double), ("comm_rate", ctypes.c_double),
+                ("storage_rate", ctypes.c_double), ("proj_a0", ctypes.c_double),
+                ("proj_b0", ctypes.c_double), ("fp64_reliable", ctypes.c_int),
+                ("seed_used", ctypes.c_uint64)]
+
+
+_P = ctypes.c_void_p
+_SZ = ctypes.c_size_t
+_I = ctypes.c_int
+
+# name -> (restype, argtypes); mirrors include/cerar.h
+SIGNATURES = {
+    "cerar_plan_create": (_I, [_I, _I, _I, ctypes.c_double, ctypes.c_uint64, ctypes.POINTER(_P)]),
+    "cerar_plan_create_desc": (_I, [ctypes.POINTER(PlanDesc), ctypes.POINTER(_P)]),
+    "cerar_plan_create_explicit": (_I, [_I, _I, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_P)]),
+    "cerar_plan_destroy": (None, [_P]),
+    "cerar_plan_get_info": (_I, [_P, ctypes.POINTER(PlanInfo)]),
+    "cerar_plan_get_matrices": (_I, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+    "cerar_chunk_len": (_I, [_P, _SZ, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]),
+    "cerar_workspace_bytes": (_I, [_P, _SZ, ctypes.POINTER(_SZ)]),
+    "cerar_slot_map": (_I, [_P, _I, ctypes.POINTER(_I)]),
+    "cerar_encode_round": (_I, [_P, _I, _SZ, _P, _SZ, _P, _SZ, _P, _P]),
+    "cerar_decode": (_I, [_P, _SZ, _P, _SZ, _P, _P, _SZ, _P]),
+    "cerar_ring_simulate": (_I, [_P, _SZ, _P, _SZ, _P, _SZ, _P, _P, _SZ, _P]),
+    "cerar_bucketed_workspace_bytes": (_I, [_P, ctypes.POINTER(_SZ), _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]),
+    "cerar_ring_simulate_bucketed": (_I, [_P, _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ), _P, _SZ, _P, _SZ,
+                                          _P, _P, _SZ, _P]),
+    "cerar_error_norms": (_I, [_I, _SZ, _P, _SZ, _P, _SZ, _P, _P]),
+    "cerar_copy_f32": (_I, [_P, _P, _SZ, _P]),
+    "cerar_last_error": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+def _hip_runtimes():
+    """Distinct HIP runtime files mapped into this process."""
+    found = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                path = line.split()[-1]
+                if "libamdhip64" in os.path.basename(path):
+                    found.add(os.path.realpath(path))
+    except OSError:
+        pass
+    return found
+
+
+def lib():
+    """The loaded in-tree libcerar.so (raises if it was not built).
+
+    torch is imported first: libcerar needs the HIP runtime by its soname
+    (libamdhip64.so.7), and once torch has loaded its runtime the dynamic
+    loader binds that soname to torch's copy, so device pointers and streams
+    from torch are valid in the library.  Two runtimes in one process would
+    not share them, so that case raises."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        import torch  # noqa: F401  (loads the HIP runtime libcerar must share)
+        handle = ctypes.CDLL(LIB_PATH)
+        runtimes = _hip_runtimes()
+        if len(runtimes) > 1:
+            raise ImportError(f"two HIP runtimes are loaded ({sorted(runtimes)}); libcerar must share torch's")
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(status):
+    if status != 0:
+        raise CerarError(status, lib().cerar_last_error().decode())
+
+
+def _dptr(a):
+    return None if a is None else ctypes.cast(a, ctypes.POINTER(ctypes.c_double))
+
+
+class Plan:
+    """Encoding/decoding plan (host fp64), see cerar_plan_create_desc."""
+
+    def __init__(self, N, c, kind, param=0.0, seed=0, base=None, perturb=None, nodes=None,
+                 eps0=0.0, als_iters=0, _handle=None):
+        L = lib()
+        self._h = _P()
+        if _handle is not None:
+            self._h = _handle
+        else:
+            keep = []
+
+            def arr(x, n):
+                if x is None:
+                    return None
+                a = np.ascontiguousarray(x, dtype=np.float64).ravel()
+                assert a.size == n, (a.size, n)
+                keep.append(a)
+                return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+            kind = _KINDS[kind] if isinstance(kind, str) else int(kind)
+            desc = PlanDesc(N, c, kind, float(param), int(seed), arr(base, N * c),
+                            arr(perturb, c * c), arr(nodes, c), float(eps0), int(als_iters))
+            _check(L.cerar_plan_create_desc(ctypes.byref(desc), ctypes.byref(self._h)))
+        info = self.info()
+        self.N, self.c, self.L = info["N"], info["c"], info["L"]
+
+    @classmethod
+    def explicit(cls, U, R):
+        U = np.ascontiguousarray(U, dtype=np.float64)
+        R = np.ascontiguousarray(R, dtype=np.float64)
+        N, c, _ = U.shape
+        h = _P()
+        _check(lib().cerar_plan_create_explicit(N, c, _dptr(U.ctypes.data), _dptr(R.ctypes.data),
+                                                ctypes.byref(h)))
+        return cls(N, c, EXPLICIT, _handle=h)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def info(self):
+        inf = PlanInfo()
+        _check(lib().cerar_plan_get_info(self._h, ctypes.byref(inf)))
+        return {name: getattr(inf, name) for name, _ in PlanInfo._fields_}
+
+    def matrices(self):
+        U = np.empty((self.N, self.c, self.c))
+        R = np.empty((self.N, self.L + 1, self.c))
+        _check(lib().cerar_plan_get_matrices(self._h, _dptr(U.ctypes.data), _dptr(R.ctypes.data)))
+        return U, R
+
+    def chunk_len(self, d):
+        p, s = _SZ(), _SZ()
+        _check(lib().cerar_chunk_len(self._h, d, ctypes.byref(p), ctypes.byref(s)))
+        return p.value, s.value
+
+    def workspace_bytes(self, d):
+        b = _SZ()
+        _check(lib().cerar_workspace_bytes(self._h, d, ctypes.byref(b)))
+        return b.value
+
+    def slot_map(self, step):
+        out = np.empty(self.N * (self.c + self.N), dtype=np.int32)
+        _check(lib().cerar_slot_map(self._h, step, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int))))
+        return out.reshape(self.N, self.c + self.N)
+
+    def bucketed_sizes(self, bucket_len):
+        lens = (_SZ * len(bucket_len))(*bucket_len)
+        wf, wb = _SZ(), _SZ()
+        _check(lib().cerar_bucketed_workspace_bytes(self._h, lens, len(bucket_len),
+                                                    ctypes.byref(wf), ctypes.byref(wb)))
+        return wf.value, wb.value
+
+    def close(self):
+        if self._h:
+            lib().cerar_plan_destroy(self._h)
+            self._h = _P()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# --- device calls (torch tensors) ----------------------------------------------
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _ld(t):
+    assert t.dim() == 2 and t.stride(1) == 1, "expected an (N, ld) row-major tensor"
+    return t.stride(0)
+
+
+def allocate(plan, d, device="cuda", work_like_grads=False):
+    """Device buffers for one all-reduce of length-d gradients: work (N, c*p),
+    ws (workspace bytes) and out (N, d)."""
+    import torch
+    p, _ = plan.chunk_len(d)
+    work = torch.empty((plan.N, plan.c * p), dtype=torch.float32, device=device)
+    ws = torch.empty(plan.workspace_bytes(d), dtype=torch.uint8, device=device)
+    out = torch.empty((plan.N, d), dtype=torch.float32, device=device)
+    return work, ws, out
+
+
+def encode_round(plan, step, d, grads, work, ws, stream=None):
+    _check(lib().cerar_encode_round(plan.handle, step, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
+                                    _ptr(ws), _stream(stream)))
+
+
+def decode(plan, d, work, ws, out, stream=None):
+    _check(lib().cerar_decode(plan.handle, d, _ptr(work), _ld(work), _ptr(ws), _ptr(out), _ld(out),
+                              _stream(stream)))
+
+
+def ring_simulate(plan, d, grads, work, ws, out, stream=None):
+    _check(lib().cerar_ring_simulate(plan.handle, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
+                                     _ptr(ws), _ptr(out), _ld(out), _stream(stream)))
+
+
+def ring_simulate_bucketed(plan, buckets, grads, work, ws, out, stream=None):
+    offs = (_SZ * len(buckets))(*[b[0] for b in buckets])
+    lens = (_SZ * len(buckets))(*[b[1] for b in buckets])
+    _check(lib().cerar_ring_simulate_bucketed(plan.handle, len(buckets), offs, lens, _ptr(grads), _ld(grads),
+                                              _ptr(work), _ld(work), _ptr(ws), _ptr(out), _ld(out),
+                                              _stream(stream)))
+
+
+def error_norms(N, d, grads, out, norms, stream=None):
+    _check(lib().cerar_error_norms(N, d, _ptr(grads), _ld(grads), _ptr(out), _ld(out), _ptr(norms),
+                                   _stream(stream)))
+
+
+def copy_f32(dst, src, stream=None):
+    assert dst.numel() == src.numel()
+    _check(lib().cerar_copy_f32(_ptr(dst), _ptr(src), dst.numel(), _stream(stream)))
+
+
+def algorithmic_bytes_per_worker(N, c, p):
+    """Bytes one worker must move under handoff sends: encode (2c+1)p,
+    rounds (4c+2N-9)p, decode (2c+N-1)p, all fp32."""
+    return (8 * c + 3 * N - 9) * p * 4
+
+
+def phase_bytes_per_worker(N, c, p):
+    """Per-launch algorithmic fp32 bytes of each phase for one worker."""
+    L = c + N - 2
+    rounds = {}
+    for k in range(1, L + 1):
+        if k <= N - 1:
+            rounds[k] = 3 * p * 4
+        elif k < L:
+            rounds[k] = (4 if k + 1 <= c else 3) * p * 4
+        else:
+            rounds[k] = 0
+    return {"encode": (2 * c + 1) * p * 4, "rounds": rounds, "decode": (2 * c + N - 1) * p * 4}
+
+
+def phase_flops_per_worker(N, c, p):
+    L = c + N - 2
+    return {"encode": 2 * c * c * p, "decode": 2 * (L + 1) * c * p}
+
+
+def isfinite(x):
+    return math.isfinite(x)

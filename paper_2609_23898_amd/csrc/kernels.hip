@@ -1,0 +1,824 @@
+// HIP kernels for gfx950 and the device-side C ABI of libcerar.
+//
+//  k_encode  (K1)  delta_{i,j} = sum_l U_i[l][j] chunk_l(g_i), all workers,
+//                  as fp32 MFMA 16x16x4 tiles: delta^T = U^T G^T, positions
+//                  on the MFMA N axis, coefficients (A operand) from LDS.
+//  k_round   (K2/K3) one ring round for all workers: next message =
+//                  received (- returning own term) (+ next own term).
+//  k_decode  (K4)  g_hat_i = Y_i R_i, the same MFMA tiling over the L+1
+//                  stored observations, gathered through the slot table.
+//  k_norms   (K5)  per-worker squared error against S = sum_w g_w, fp64.
+//  k_copy          plain streaming copy (bandwidth reference).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "cerar_internal.hpp"
+
+namespace cerar {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;                  // 4 wavefronts of 64
+constexpr int kWaves = kThreads / 64;
+constexpr size_t kLdsBudget = 64 * 1024;       // bytes of LDS a workgroup may use
+
+// Address of a p-float slot (see RingTables): the workers' own chunks in
+// `work`, or the per-worker message pool in the workspace.
+struct SlotBase {
+    float *work;
+    size_t ld_work;
+    size_t p;
+    float *pool;
+    size_t pool_stride;
+    int Nc;
+    int c;
+    __device__ __host__ float *ptr(int s) const {
+        return s < Nc ? work + (size_t)(s / c) * ld_work + (size_t)(s % c) * p
+                      : pool + (size_t)(s - Nc) * pool_stride;
+    }
+};
+
+// ---- position-tile I/O -------------------------------------------------------
+// A wave covers 64 consecutive positions e0..e0+63 of one p-float row.  In the
+// vector layout lane (krow, col) holds positions e0 + 4 col + t, t = 0..3, and
+// MFMA number t works on component t; in the scalar layout MFMA t works on
+// position e0 + 16 t + col.  Entries at or beyond `limit` (flat index
+// row_off + pos) read as zero.
+
+template <bool VEC>
+__device__ inline v4f load_tile(const float *__restrict__ row, size_t row_off, size_t e0, int col,
+                                size_t p, size_t limit) {
+    v4f v = {0.f, 0.f, 0.f, 0.f};
+    if (VEC) {
+        const size_t pos = e0 + 4 * (size_t)col;
+        if (pos < p) {
+            const size_t flat = row_off + pos;
+            if (flat + 3 < limit) {
+                v = *reinterpret_cast<const v4f *>(row + pos);
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if (flat + t < limit) v[t] = row[pos + t];
+            }
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const size_t pos = e0 + 16 * (size_t)t + col;
+            if (pos < p && row_off + pos < limit) v[t] = row[pos];
+        }
+    }
+    return v;
+}
+
+template <bool VEC>
+__device__ inline void store_tile(float *__restrict__ row, size_t row_off, size_t e0, int col, size_t p,
+                                  size_t limit, v4f v) {
+    if (VEC) {
+        const size_t pos = e0 + 4 * (size_t)col;
+        if (pos < p) {
+            const size_t flat = row_off + pos;
+            if (flat + 3 < limit) {
+                *reinterpret_cast<v4f *>(row + pos) = v;
+            } else {
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    if (flat + t < limit) row[pos + t] = v[t];
+            }
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const size_t pos = e0 + 16 * (size_t)t + col;
+            if (pos < p && row_off + pos < limit) row[pos] = v[t];
+        }
+    }
+}
+
+// ---- K1: encode -----------------------------------------------------------------
+
+struct EncParams {
+    const float *grads;
+    size_t ld_g;
+    size_t d;
+    SlotBase sb;
+    const float *frag;      // N x MT x KSe x 64
+    int N, c, MT, KSe;
+    int mt0, mt1;           // M-tiles handled by this launch
+    int wg_per_worker;
+    size_t nblk;            // 64-position blocks per row
+};
+
+template <int KS, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
+    extern __shared__ float sfrag[];
+    const int worker = blockIdx.x / a.wg_per_worker;
+    const int wg = blockIdx.x - worker * a.wg_per_worker;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, krow = lane >> 4;
+    const int nmt = a.mt1 - a.mt0;
+    const float *gfrag = a.frag + ((size_t)worker * a.MT + a.mt0) * a.KSe * 64;
+    for (int t = threadIdx.x; t < nmt * a.KSe * 64; t += kThreads) sfrag[t] = gfrag[t];
+    __syncthreads();
+    const float *src = a.grads + (size_t)worker * a.ld_g;
+    float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
+    float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;   // worker's first pool slot
+    const size_t p = a.sb.p;
+    for (size_t blk = (size_t)wg * kWaves + wave; blk < a.nblk; blk += (size_t)a.wg_per_worker * kWaves) {
+        const size_t e0 = blk * 64;
+        v4f b[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int l = ks * 4 + krow;
+            if (ks < a.KSe && l < a.c)
+                b[ks] = load_tile<VEC>(src + (size_t)l * p, (size_t)l * p, e0, col, p, a.d);
+            else
+                b[ks] = v4f{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int mt = 0; mt < nmt; ++mt) {
+            v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0, acc2 = acc0, acc3 = acc0;
+            const float *fr = sfrag + (size_t)mt * a.KSe * 64 + lane;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                if (ks < a.KSe) {
+                    const float av = fr[ks * 64];
+                    acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][0], acc0, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][1], acc1, 0, 0, 0);
+                    acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][2], acc2, 0, 0, 0);
+                    acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][3], acc3, 0, 0, 0);
+                }
+            }
+            // D fragment: lane (krow, col), register r holds output row 4 krow + r.
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int j = (a.mt0 + mt) * 16 + krow * 4 + r;
+                if (j < a.c) {
+                    const v4f v = {acc0[r], acc1[r], acc2[r], acc3[r]};
+                    store_tile<VEC>(dst + (size_t)j * p, 0, e0, col, p, p, v);
+                    if (j == 0) store_tile<VEC>(x1, 0, e0, col, p, p, v);
+                }
+            }
+        }
+    }
+}
+
+// ---- K2/K3: one ring round ---------------------------------------------------
+// MODE 0: x_next = recv + add            (rounds 1..N-1)
+// MODE 1: x_next = (recv - sub) + add    (rounds N..c-1)
+// MODE 2: x_next = recv - sub            (rounds c..L-1)
+
+struct RoundParams {
+    SlotBase sb;
+    const RoundOp *ops;     // N entries of this round
+    int wg_per_worker;
+};
+
+constexpr int kRoundUnroll = 4;
+
+template <int MODE, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_round(RoundParams a) {
+    const int worker = blockIdx.x / a.wg_per_worker;
+    const int wg = blockIdx.x - worker * a.wg_per_worker;
+    const RoundOp op = a.ops[worker];
+    const float *__restrict__ recv = a.sb.ptr(op.recv);
+    const float *sub = MODE >= 1 ? a.sb.ptr(op.sub) : nullptr;   // aliases dst (in place)
+    const float *__restrict__ add = MODE <= 1 ? a.sb.ptr(op.add) : nullptr;
+    float *dst = a.sb.ptr(op.dst);
+    const size_t p = a.sb.p;
+    const size_t stride = (size_t)a.wg_per_worker * kThreads * kRoundUnroll;
+    if (VEC) {
+        const size_t n4 = p / 4;
+        const v4f *r4 = reinterpret_cast<const v4f *>(recv);
+        const v4f *s4 = reinterpret_cast<const v4f *>(sub);
+        const v4f *a4 = reinterpret_cast<const v4f *>(add);
+        v4f *d4 = reinterpret_cast<v4f *>(dst);
+        for (size_t base = (size_t)wg * kThreads * kRoundUnroll + threadIdx.x; base < n4; base += stride) {
+            v4f x[kRoundUnroll], y[kRoundUnroll], z[kRoundUnroll];
+#pragma unroll
+            for (int u = 0; u < kRoundUnroll; ++u) {
+                const size_t i = base + (size_t)u * kThreads;
+                if (i < n4) {
+                    x[u] = r4[i];
+                    if (MODE >= 1) y[u] = s4[i];
+                    if (MODE <= 1) z[u] = a4[i];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kRoundUnroll; ++u) {
+                const size_t i = base + (size_t)u * kThreads;
+                if (i < n4) {
+                    v4f v = x[u];
+                    if (MODE >= 1) v = v - y[u];
+                    if (MODE <= 1) v = v + z[u];
+                    d4[i] = v;
+                }
+            }
+        }
+    } else {
+        for (size_t base = (size_t)wg * kThreads * kRoundUnroll + threadIdx.x; base < p; base += stride) {
+#pragma unroll
+            for (int u = 0; u < kRoundUnroll; ++u) {
+                const size_t i = base + (size_t)u * kThreads;
+                if (i < p) {
+                    float v = recv[i];
+                    if (MODE >= 1) v = v - sub[i];
+                    if (MODE <= 1) v = v + add[i];
+                    dst[i] = v;
+                }
+            }
+        }
+    }
+}
+
+// ---- K4: decode ----------------------------------------------------------------
+
+struct DecParams {
+    SlotBase sb;
+    const int *ycols;       // N x K slot ids
+    float *out;
+    size_t ld_o;
+    size_t d;
+    const float *frag;      // N x MT x KSd x 64
+    int N, c, K, MT, KSd;
+    int mt0, mt1;
+    int wg_per_worker;
+    size_t nblk;
+};
+
+template <int KS, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
+    extern __shared__ float smem[];
+    const int worker = blockIdx.x / a.wg_per_worker;
+    const int wg = blockIdx.x - worker * a.wg_per_worker;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, krow = lane >> 4;
+    const int nmt = a.mt1 - a.mt0;
+    const size_t nfrag = (size_t)nmt * a.KSd * 64;
+    float *sfrag = smem;
+    const float **srow = reinterpret_cast<const float **>(smem + ((nfrag + 1) & ~(size_t)1));
+    const float *gfrag = a.frag + ((size_t)worker * a.MT + a.mt0) * a.KSd * 64;
+    for (size_t t = threadIdx.x; t < nfrag; t += kThreads) sfrag[t] = gfrag[t];
+    for (int t = threadIdx.x; t < a.K; t += kThreads) srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + t]);
+    __syncthreads();
+    float *out = a.out + (size_t)worker * a.ld_o;
+    const size_t p = a.sb.p;
+    for (size_t blk = (size_t)wg * kWaves + wave; blk < a.nblk; blk += (size_t)a.wg_per_worker * kWaves) {
+        const size_t e0 = blk * 64;
+        v4f b[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int k = ks * 4 + krow;
+            if (ks < a.KSd && k < a.K)
+                b[ks] = load_tile<VEC>(srow[k], 0, e0, col, p, p);
+            else
+                b[ks] = v4f{0.f, 0.f, 0.f, 0.f};
+        }
+        for (int mt = 0; mt < nmt; ++mt) {
+            v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0, acc2 = acc0, acc3 = acc0;
+            const float *fr = sfrag + (size_t)mt * a.KSd * 64 + lane;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                if (ks < a.KSd) {
+                    const float av = fr[ks * 64];
+                    acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][0], acc0, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][1], acc1, 0, 0, 0);
+                    acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][2], acc2, 0, 0, 0);
+                    acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][3], acc3, 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = (a.mt0 + mt) * 16 + krow * 4 + r;
+                if (m < a.c) {
+                    const v4f v = {acc0[r], acc1[r], acc2[r], acc3[r]};
+                    store_tile<VEC>(out + (size_t)m * p, (size_t)m * p, e0, col, p, a.d, v);
+                }
+            }
+        }
+    }
+}
+
+// ---- K5: error norms ---------------------------------------------------------
+
+constexpr int kNormWorkers = 8;
+
+__global__ void k_fill_zero(double *x, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) x[i] = 0.0;
+}
+
+__device__ inline double wave_sum(double v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
+    return v;
+}
+
+__global__ __launch_bounds__(kThreads) void k_norms(int N, size_t d, const float *__restrict__ grads,
+                                                   size_t ld_g, const float *__restrict__ out, size_t ld_o,
+                                                   double *norms) {
+    __shared__ double red[kWaves][kNormWorkers + 1];
+    const int w0 = blockIdx.y * kNormWorkers;
+    double acc[kNormWorkers + 1];
+#pragma unroll
+    for (int q = 0; q <= kNormWorkers; ++q) acc[q] = 0.0;
+    for (size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x; e < d; e += (size_t)gridDim.x * kThreads) {
+        double S = 0.0;
+        for (int w = 0; w < N; ++w) S += (double)grads[(size_t)w * ld_g + e];
+        acc[kNormWorkers] += S * S;
+#pragma unroll
+        for (int q = 0; q < kNormWorkers; ++q) {
+            const int w = w0 + q;
+            if (w < N) {
+                const double diff = (double)out[(size_t)w * ld_o + e] - S;
+                acc[q] += diff * diff;
+            }
+        }
+    }
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int q = 0; q <= kNormWorkers; ++q) {
+        const double v = wave_sum(acc[q]);
+        if (lane == 0) red[wave][q] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x <= kNormWorkers) {
+        const int q = threadIdx.x;
+        double v = 0.0;
+        for (int w = 0; w < kWaves; ++w) v += red[w][q];
+        if (q < kNormWorkers) {
+            if (w0 + q < N) atomicAdd(norms + w0 + q, v);
+        } else if (blockIdx.y == 0) {
+            atomicAdd(norms + N, v);
+        }
+    }
+}
+
+// ---- copy ----------------------------------------------------------------------
+
+__global__ __launch_bounds__(kThreads) void k_copy4(v4f *__restrict__ dst, const v4f *__restrict__ src, size_t n4) {
+    const size_t stride = (size_t)gridDim.x * kThreads * kRoundUnroll;
+    for (size_t base = (size_t)blockIdx.x * kThreads * kRoundUnroll + threadIdx.x; base < n4; base += stride) {
+        v4f x[kRoundUnroll];
+#pragma unroll
+        for (int u = 0; u < kRoundUnroll; ++u) {
+            const size_t i = base + (size_t)u * kThreads;
+            if (i < n4) x[u] = src[i];
+        }
+#pragma unroll
+        for (int u = 0; u < kRoundUnroll; ++u) {
+            const size_t i = base + (size_t)u * kThreads;
+            if (i < n4) dst[i] = x[u];
+        }
+    }
+}
+
+__global__ void k_copy1(float *__restrict__ dst, const float *__restrict__ src, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+// ---- host helpers ----------------------------------------------------------------
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(CERAR_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                         \
+    do {                                            \
+        hipError_t _e = (expr);                     \
+        if (_e != hipSuccess) return hip_fail(_e, what); \
+    } while (0)
+
+template <class T>
+int upload(T **dst, const T *src, size_t count) {
+    HIP_TRY(hipMalloc((void **)dst, count * sizeof(T)), "hipMalloc (plan coefficients)");
+    HIP_TRY(hipMemcpy(*dst, src, count * sizeof(T), hipMemcpyHostToDevice), "hipMemcpy (plan coefficients)");
+    return CERAR_OK;
+}
+
+// Fp32 fragments and tables of the plan on the current device (uploaded once).
+int device_copy(const cerar_plan *plan, const DeviceCopy **out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> g(plan->dev_mu);
+    auto it = plan->dev.find(dev);
+    if (it != plan->dev.end()) {
+        *out = &it->second;
+        return CERAR_OK;
+    }
+    DeviceCopy dc;
+    int st = upload(&dc.enc_frag, plan->enc_frag.data(), plan->enc_frag.size());
+    if (!st) st = upload(&dc.dec_frag, plan->dec_frag.data(), plan->dec_frag.size());
+    if (!st) st = upload(&dc.ycols, plan->tab.ycols.data(), plan->tab.ycols.size());
+    if (!st) st = upload(&dc.rounds, plan->tab.rounds.data(), plan->tab.rounds.size());
+    if (st) {
+        (void)hipFree(dc.enc_frag);
+        (void)hipFree(dc.dec_frag);
+        (void)hipFree(dc.ycols);
+        (void)hipFree(dc.rounds);
+        return st;
+    }
+    *out = &(plan->dev[dev] = dc);
+    return CERAR_OK;
+}
+
+// Next expected step per workspace (cerar_encode_round ordering).
+std::mutex g_cursor_mu;
+std::map<const void *, std::pair<const cerar_plan *, int>> g_cursor;
+
+bool aligned16(const void *ptr) { return ((uintptr_t)ptr & 15) == 0; }
+
+bool overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
+    const char *pa = (const char *)a, *pb = (const char *)b;
+    return pa < pb + bbytes && pb < pa + abytes;
+}
+
+struct Geometry {
+    size_t p, pool_stride;
+    bool vec;
+};
+
+int check_common(const cerar_plan *plan, size_t d, const void *work, size_t ld_work, const void *ws,
+                 Geometry &g) {
+    if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
+    if (d == 0) return fail(CERAR_E_INVAL, "d must be > 0");
+    if (!work || !ws) return fail(CERAR_E_INVAL, "work and ws must be non-NULL");
+    int st = cerar_chunk_len(plan, d, &g.p, &g.pool_stride);
+    if (st) return st;
+    if (ld_work < (size_t)plan->c * g.p)
+        return fail(CERAR_E_INVAL, "ld_work=%zu < c*p=%zu", ld_work, (size_t)plan->c * g.p);
+    g.vec = (g.p % 4 == 0) && (ld_work % 4 == 0) && aligned16(work) && aligned16(ws);
+    return CERAR_OK;
+}
+
+SlotBase slot_base(const cerar_plan *plan, const Geometry &g, float *work, size_t ld_work, void *ws) {
+    return SlotBase{work, ld_work, g.p, (float *)ws, g.pool_stride, plan->N * plan->c, plan->c};
+}
+
+int wg_for(size_t nblk) {
+    // 64-position blocks per workgroup pass = 4 (one per wave); ~8 passes each
+    size_t w = (nblk + 4 * 8 - 1) / (4 * 8);
+    if (w < 1) w = 1;
+    if (w > 16384) w = 16384;
+    return (int)w;
+}
+
+template <int KS>
+void launch_encode_ks(const EncParams &a, bool vec, size_t lds, hipStream_t s, dim3 grid) {
+    if (vec) hipLaunchKernelGGL((k_encode<KS, true>), grid, dim3(kThreads), lds, s, a);
+    else hipLaunchKernelGGL((k_encode<KS, false>), grid, dim3(kThreads), lds, s, a);
+}
+
+template <int KS>
+void launch_decode_ks(const DecParams &a, bool vec, size_t lds, hipStream_t s, dim3 grid) {
+    if (vec) hipLaunchKernelGGL((k_decode<KS, true>), grid, dim3(kThreads), lds, s, a);
+    else hipLaunchKernelGGL((k_decode<KS, false>), grid, dim3(kThreads), lds, s, a);
+}
+
+// M-tiles per launch so that their fragments fit the LDS budget.
+int mtiles_per_launch(int MT, int KS, size_t extra) {
+    size_t per = (size_t)KS * 64 * sizeof(float);
+    int n = (int)((kLdsBudget - extra) / per);
+    return std::max(1, std::min(MT, n));
+}
+
+int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, size_t d,
+                   const float *grads, size_t ld_grads, float *work, size_t ld_work, void *ws, hipStream_t s) {
+    EncParams a;
+    a.grads = grads;
+    a.ld_g = ld_grads;
+    a.d = d;
+    a.sb = slot_base(plan, g, work, ld_work, ws);
+    a.frag = dc->enc_frag;
+    a.N = plan->N;
+    a.c = plan->c;
+    a.MT = plan->MT;
+    a.KSe = plan->KSe;
+    a.nblk = (g.p + 63) / 64;
+    a.wg_per_worker = wg_for(a.nblk);
+    const bool vec = g.vec && (ld_grads % 4 == 0) && aligned16(grads);
+    const dim3 grid((unsigned)(plan->N * a.wg_per_worker));
+    const int step = mtiles_per_launch(plan->MT, plan->KSe, 0);
+    for (int mt0 = 0; mt0 < plan->MT; mt0 += step) {
+        a.mt0 = mt0;
+        a.mt1 = std::min(plan->MT, mt0 + step);
+        const size_t lds = (size_t)(a.mt1 - a.mt0) * plan->KSe * 64 * sizeof(float);
+        const int ks = plan->KSe;
+        if (ks <= 1) launch_encode_ks<1>(a, vec, lds, s, grid);
+        else if (ks <= 2) launch_encode_ks<2>(a, vec, lds, s, grid);
+        else if (ks <= 4) launch_encode_ks<4>(a, vec, lds, s, grid);
+        else if (ks <= 8) launch_encode_ks<8>(a, vec, lds, s, grid);
+        else if (ks <= 16) launch_encode_ks<16>(a, vec, lds, s, grid);
+        else if (ks <= 24) launch_encode_ks<24>(a, vec, lds, s, grid);
+        else launch_encode_ks<32>(a, vec, lds, s, grid);
+        HIP_TRY(hipGetLastError(), "launch encode");
+    }
+    return CERAR_OK;
+}
+
+int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, int k, float *work,
+                  size_t ld_work, void *ws, hipStream_t s) {
+    const int N = plan->N, c = plan->c, L = plan->L;
+    if (k == L) return CERAR_OK;                     // the last round only relabels
+    RoundParams a;
+    a.sb = slot_base(plan, g, work, ld_work, ws);
+    a.ops = dc->rounds + (size_t)k * N;
+    const size_t units = g.vec ? g.p / 4 : g.p;
+    size_t w = (units + (size_t)kThreads * kRoundUnroll - 1) / ((size_t)kThreads * kRoundUnroll);
+    a.wg_per_worker = (int)std::max<size_t>(1, std::min<size_t>(w, 1 << 20));
+    const dim3 grid((unsigned)(N * a.wg_per_worker));
+    const int mode = (k <= N - 1) ? 0 : (k + 1 <= c ? 1 : 2);
+    if (g.vec) {
+        if (mode == 0) hipLaunchKernelGGL((k_round<0, true>), grid, dim3(kThreads), 0, s, a);
+        else if (mode == 1) hipLaunchKernelGGL((k_round<1, true>), grid, dim3(kThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_round<2, true>), grid, dim3(kThreads), 0, s, a);
+    } else {
+        if (mode == 0) hipLaunchKernelGGL((k_round<0, false>), grid, dim3(kThreads), 0, s, a);
+        else if (mode == 1) hipLaunchKernelGGL((k_round<1, false>), grid, dim3(kThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_round<2, false>), grid, dim3(kThreads), 0, s, a);
+    }
+    HIP_TRY(hipGetLastError(), "launch round");
+    return CERAR_OK;
+}
+
+int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, size_t d,
+                   const float *work, size_t ld_work, const void *ws, float *out, size_t ld_out, hipStream_t s) {
+    DecParams a;
+    a.sb = slot_base(plan, g, const_cast<float *>(work), ld_work, const_cast<void *>(ws));
+    a.ycols = dc->ycols;
+    a.out = out;
+    a.ld_o = ld_out;
+    a.d = d;
+    a.frag = dc->dec_frag;
+    a.N = plan->N;
+    a.c = plan->c;
+    a.K = plan->L + 1;
+    a.MT = plan->MT;
+    a.KSd = plan->KSd;
+    a.nblk = (g.p + 63) / 64;
+    a.wg_per_worker = wg_for(a.nblk);
+    const bool vec = g.vec && (ld_out % 4 == 0) && aligned16(out);
+    const dim3 grid((unsigned)(plan->N * a.wg_per_worker));
+    const size_t rows_bytes = (size_t)a.K * sizeof(float *) + 16;
+    const int step = mtiles_per_launch(plan->MT, plan->KSd, rows_bytes);
+    for (int mt0 = 0; mt0 < plan->MT; mt0 += step) {
+        a.mt0 = mt0;
+        a.mt1 = std::min(plan->MT, mt0 + step);
+        const size_t lds = (size_t)(a.mt1 - a.mt0) * plan->KSd * 64 * sizeof(float) + rows_bytes;
+        const int ks = plan->KSd;
+        if (ks <= 4) launch_decode_ks<4>(a, vec, lds, s, grid);
+        else if (ks <= 8) launch_decode_ks<8>(a, vec, lds, s, grid);
+        else if (ks <= 12) launch_decode_ks<12>(a, vec, lds, s, grid);
+        else if (ks <= 16) launch_decode_ks<16>(a, vec, lds, s, grid);
+        else if (ks <= 20) launch_decode_ks<20>(a, vec, lds, s, grid);
+        else if (ks <= 24) launch_decode_ks<24>(a, vec, lds, s, grid);
+        else if (ks <= 32) launch_decode_ks<32>(a, vec, lds, s, grid);
+        else if (ks <= 40) launch_decode_ks<40>(a, vec, lds, s, grid);
+        else launch_decode_ks<48>(a, vec, lds, s, grid);
+        HIP_TRY(hipGetLastError(), "launch decode");
+    }
+    return CERAR_OK;
+}
+
+int check_grads(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads, const float *work,
+                size_t ld_work, const Geometry &g) {
+    if (!grads) return fail(CERAR_E_INVAL, "grads is NULL");
+    if (ld_grads < d) return fail(CERAR_E_INVAL, "ld_grads=%zu < d=%zu", ld_grads, d);
+    const size_t N = plan->N;
+    if ((const void *)grads == (const void *)work) {
+        if (ld_grads != ld_work) return fail(CERAR_E_INVAL, "in-place encode needs ld_grads == ld_work");
+    } else if (overlap(grads, ((N - 1) * ld_grads + d) * sizeof(float), work,
+                       ((N - 1) * ld_work + plan->c * g.p) * sizeof(float))) {
+        return fail(CERAR_E_INVAL, "grads and work overlap without being the same buffer");
+    }
+    return CERAR_OK;
+}
+
+int check_out(const cerar_plan *plan, size_t d, const float *work, size_t ld_work, const void *ws,
+              const float *out, size_t ld_out, const Geometry &g) {
+    if (!out) return fail(CERAR_E_INVAL, "out is NULL");
+    if (ld_out < d) return fail(CERAR_E_INVAL, "ld_out=%zu < d=%zu", ld_out, d);
+    const size_t N = plan->N;
+    const size_t out_bytes = ((N - 1) * ld_out + d) * sizeof(float);
+    if (overlap(out, out_bytes, work, ((N - 1) * ld_work + plan->c * g.p) * sizeof(float)) ||
+        overlap(out, out_bytes, ws, (size_t)plan->tab.pool_slots() * g.pool_stride * sizeof(float)))
+        return fail(CERAR_E_INVAL, "out overlaps work or ws");
+    return CERAR_OK;
+}
+
+}  // namespace
+
+void release_device(cerar_plan *plan) {
+    std::lock_guard<std::mutex> g(plan->dev_mu);
+    int cur = 0;
+    bool have = hipGetDevice(&cur) == hipSuccess;
+    for (auto &kv : plan->dev) {
+        if (have) (void)hipSetDevice(kv.first);
+        (void)hipFree(kv.second.enc_frag);
+        (void)hipFree(kv.second.dec_frag);
+        (void)hipFree(kv.second.ycols);
+        (void)hipFree(kv.second.rounds);
+    }
+    if (have) (void)hipSetDevice(cur);
+    plan->dev.clear();
+    std::lock_guard<std::mutex> c(g_cursor_mu);
+    for (auto it = g_cursor.begin(); it != g_cursor.end();)
+        it = it->second.first == plan ? g_cursor.erase(it) : std::next(it);
+}
+
+}  // namespace cerar
+
+using namespace cerar;
+
+extern "C" int cerar_encode_round(const cerar_plan *plan, int step, size_t d, const float *grads,
+                                  size_t ld_grads, float *work, size_t ld_work, void *ws, cerar_stream stream) {
+    clear_error();
+    Geometry g;
+    int st = check_common(plan, d, work, ld_work, ws, g);
+    if (st) return st;
+    if (step < 0 || step > plan->L) return fail(CERAR_E_INVAL, "step %d outside [0, L=%d]", step, plan->L);
+    if (step == 0) {
+        st = check_grads(plan, d, grads, ld_grads, work, ld_work, g);
+        if (st) return st;
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_cursor_mu);
+        auto it = g_cursor.find(ws);
+        if (step > 0 && (it == g_cursor.end() || it->second.first != plan || it->second.second != step))
+            return fail(CERAR_E_STATE, "step %d called out of order on this workspace", step);
+    }
+    const DeviceCopy *dc;
+    st = device_copy(plan, &dc);
+    if (st) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    st = step == 0 ? enqueue_encode(plan, dc, g, d, grads, ld_grads, work, ld_work, ws, s)
+                   : enqueue_round(plan, dc, g, step, work, ld_work, ws, s);
+    if (st) return st;
+    std::lock_guard<std::mutex> lk(g_cursor_mu);
+    g_cursor[ws] = {plan, step + 1};
+    return CERAR_OK;
+}
+
+extern "C" int cerar_decode(const cerar_plan *plan, size_t d, const float *work, size_t ld_work, const void *ws,
+                            float *out, size_t ld_out, cerar_stream stream) {
+    clear_error();
+    Geometry g;
+    int st = check_common(plan, d, work, ld_work, ws, g);
+    if (st) return st;
+    st = check_out(plan, d, work, ld_work, ws, out, ld_out, g);
+    if (st) return st;
+    {
+        std::lock_guard<std::mutex> lk(g_cursor_mu);
+        auto it = g_cursor.find(ws);
+        if (it == g_cursor.end() || it->second.first != plan || it->second.second != plan->L + 1)
+            return fail(CERAR_E_STATE, "decode before rounds 1..L completed on this workspace");
+    }
+    const DeviceCopy *dc;
+    st = device_copy(plan, &dc);
+    if (st) return st;
+    return enqueue_decode(plan, dc, g, d, work, ld_work, ws, out, ld_out, reinterpret_cast<hipStream_t>(stream));
+}
+
+extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                   float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
+                                   cerar_stream stream) {
+    clear_error();
+    Geometry g;
+    int st = check_common(plan, d, work, ld_work, ws, g);
+    if (st) return st;
+    st = check_grads(plan, d, grads, ld_grads, work, ld_work, g);
+    if (st) return st;
+    st = check_out(plan, d, work, ld_work, ws, out, ld_out, g);
+    if (st) return st;
+    const DeviceCopy *dc;
+    st = device_copy(plan, &dc);
+    if (st) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    st = enqueue_encode(plan, dc, g, d, grads, ld_grads, work, ld_work, ws, s);
+    for (int k = 1; k <= plan->L && !st; ++k) st = enqueue_round(plan, dc, g, k, work, ld_work, ws, s);
+    if (!st) st = enqueue_decode(plan, dc, g, d, work, ld_work, ws, out, ld_out, s);
+    if (st) return st;
+    std::lock_guard<std::mutex> lk(g_cursor_mu);
+    g_cursor[ws] = {plan, plan->L + 1};
+    return CERAR_OK;
+}
+
+extern "C" int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_grads, const float *out,
+                                 size_t ld_out, double *norms, cerar_stream stream) {
+    clear_error();
+    if (N < 1 || N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [1, %d]", N, kMaxN);
+    if (d == 0 || !grads || !out || !norms) return fail(CERAR_E_INVAL, "d > 0 and non-NULL buffers required");
+    if (ld_grads < d || ld_out < d) return fail(CERAR_E_INVAL, "strides must be >= d");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k_fill_zero, dim3(1), dim3(128), 0, s, norms, N + 1);
+    HIP_TRY(hipGetLastError(), "launch fill");
+    size_t blocks = (d + kThreads - 1) / kThreads;
+    blocks = std::min<size_t>(blocks, 4096);
+    const dim3 grid((unsigned)blocks, (unsigned)((N + kNormWorkers - 1) / kNormWorkers));
+    hipLaunchKernelGGL(k_norms, grid, dim3(kThreads), 0, s, N, d, grads, ld_grads, out, ld_out, norms);
+    HIP_TRY(hipGetLastError(), "launch norms");
+    return CERAR_OK;
+}
+
+extern "C" int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stream stream) {
+    clear_error();
+    if (!dst || !src) return fail(CERAR_E_INVAL, "NULL buffer");
+    if (n == 0) return CERAR_OK;
+    if (overlap(dst, n * sizeof(float), src, n * sizeof(float))) return fail(CERAR_E_INVAL, "buffers overlap");
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (n % 4 == 0 && aligned16(dst) && aligned16(src)) {
+        const size_t n4 = n / 4;
+        size_t blocks = (n4 + (size_t)kThreads * kRoundUnroll - 1) / ((size_t)kThreads * kRoundUnroll);
+        blocks = std::max<size_t>(1, std::min<size_t>(blocks, 1 << 20));
+        hipLaunchKernelGGL(k_copy4, dim3((unsigned)blocks), dim3(kThreads), 0, s, (v4f *)dst, (const v4f *)src, n4);
+    } else {
+        size_t blocks = std::max<size_t>(1, std::min<size_t>((n + kThreads - 1) / kThreads, 1 << 16));
+        hipLaunchKernelGGL(k_copy1, dim3((unsigned)blocks), dim3(kThreads), 0, s, dst, src, n);
+    }
+    HIP_TRY(hipGetLastError(), "launch copy");
+    return CERAR_OK;
+}
+
+namespace {
+
+struct BucketLayout {
+    size_t p, stride, work_off, ws_off;
+};
+
+int bucket_layout(const cerar_plan *plan, int nb, const size_t *len, std::vector<BucketLayout> &lay,
+                  size_t &work_floats, size_t &ws_bytes) {
+    if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
+    if (nb < 1 || !len) return fail(CERAR_E_INVAL, "need at least one bucket");
+    lay.resize(nb);
+    work_floats = 0;
+    ws_bytes = 0;
+    for (int b = 0; b < nb; ++b) {
+        if (len[b] == 0) return fail(CERAR_E_INVAL, "bucket %d is empty", b);
+        BucketLayout &B = lay[b];
+        B.p = (len[b] + plan->c - 1) / plan->c;
+        B.stride = (B.p + 63) / 64 * 64;
+        B.work_off = work_floats;
+        B.ws_off = ws_bytes;
+        work_floats += (size_t)plan->c * B.p;
+        ws_bytes += (size_t)plan->tab.pool_slots() * B.stride * sizeof(float);
+    }
+    return CERAR_OK;
+}
+
+}  // namespace
+
+extern "C" int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len, int nbuckets,
+                                              size_t *work_floats, size_t *ws_bytes) {
+    clear_error();
+    if (!work_floats || !ws_bytes) return fail(CERAR_E_INVAL, "NULL output");
+    std::vector<BucketLayout> lay;
+    return bucket_layout(plan, nbuckets, bucket_len, lay, *work_floats, *ws_bytes);
+}
+
+extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets, const size_t *bucket_off,
+                                            const size_t *bucket_len, const float *grads, size_t ld_grads,
+                                            float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
+                                            cerar_stream stream) {
+    clear_error();
+    std::vector<BucketLayout> lay;
+    size_t work_floats, ws_bytes;
+    int st = bucket_layout(plan, nbuckets, bucket_len, lay, work_floats, ws_bytes);
+    if (st) return st;
+    if (!bucket_off || !grads || !work || !ws || !out) return fail(CERAR_E_INVAL, "NULL argument");
+    if (ld_work < work_floats) return fail(CERAR_E_INVAL, "ld_work=%zu < %zu floats of bucket slots", ld_work, work_floats);
+    size_t span = 0;
+    for (int b = 0; b < nbuckets; ++b) span = std::max(span, bucket_off[b] + bucket_len[b]);
+    if (ld_grads < span || ld_out < span) return fail(CERAR_E_INVAL, "ld_grads and ld_out must cover every bucket");
+    const size_t N = plan->N;
+    const size_t out_bytes = ((N - 1) * ld_out + span) * sizeof(float);
+    const size_t work_bytes = ((N - 1) * ld_work + work_floats) * sizeof(float);
+    if (overlap(out, out_bytes, work, work_bytes) || overlap(out, out_bytes, ws, ws_bytes))
+        return fail(CERAR_E_INVAL, "out overlaps work or ws");
+    if (overlap(grads, ((N - 1) * ld_grads + span) * sizeof(float), work, work_bytes))
+        return fail(CERAR_E_INVAL, "bucketed encode is out of place: grads and work must not overlap");
+    const DeviceCopy *dc;
+    st = device_copy(plan, &dc);
+    if (st) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    for (int b = 0; b < nbuckets && !st; ++b) {
+        const BucketLayout &B = lay[b];
+        Geometry g;
+        g.p = B.p;
+        g.pool_stride = B.stride;
+        float *wb = work + B.work_off;
+        void *sb = (char *)ws + B.ws_off;
+        g.vec = (g.p % 4 == 0) && (ld_work % 4 == 0) && aligned16(wb) && aligned16(sb);
+        const float *gb = grads + bucket_off[b];
+        float *ob = out + bucket_off[b];
+        st = enqueue_encode(plan, dc, g, bucket_len[b], gb, ld_grads, wb, ld_work, sb, s);
+        for (int k = 1; k <= plan->L && !st; ++k) st = enqueue_round(plan, dc, g, k, wb, ld_work, sb, s);
+        if (!st) st = enqueue_decode(plan, dc, g, bucket_len[b], wb, ld_work, sb, ob, ld_out, s);
+    }
+    return st;
+}

@@ -1,0 +1,617 @@
+// Host fp64 plan construction for CERAR (Sec. II-B to II-D) and the
+// slot-ownership tables of the single-GPU handoff ring.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <set>
+#include <thread>
+
+#include "cerar_internal.hpp"
+#include "linalg.hpp"
+
+namespace cerar {
+
+static thread_local std::string g_last_error;
+
+int fail(int status, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
+void clear_error() { g_last_error.clear(); }
+
+namespace {
+
+const double kNaN = std::numeric_limits<double>::quiet_NaN();
+
+// ---- seeded base matrix: splitmix64 (Steele, Lea & Flood 2014) + Box-Muller
+struct SplitMix64 {
+    uint64_t state;
+    uint64_t next() {
+        uint64_t z = (state += 0x9E3779B97F4A7C15ull);
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+        return z ^ (z >> 31);
+    }
+    double uniform() { return ((double)(next() >> 11) + 0.5) * 0x1.0p-53; }
+};
+
+std::vector<double> gaussian_base(uint64_t seed, int N, int c) {
+    SplitMix64 g{seed};
+    std::vector<double> B((size_t)N * c);
+    for (size_t i = 0; i < B.size(); i += 2) {
+        const double r = std::sqrt(-2.0 * std::log(g.uniform()));
+        const double th = 2.0 * M_PI * g.uniform();
+        B[i] = r * std::cos(th);
+        if (i + 1 < B.size()) B[i + 1] = r * std::sin(th);
+    }
+    return B;
+}
+
+std::vector<double> chebyshev_nodes(int c) {
+    std::vector<double> x(c);
+    for (int j = 1; j <= c; ++j) x[j - 1] = std::cos((2.0 * j - 1.0) * M_PI / (2.0 * c));
+    return x;
+}
+
+// Runs f(k) for k in [0, n) on up to hardware_concurrency threads.
+template <class F>
+void parallel_for(int n, F f) {
+    int nt = (int)std::min<unsigned>(std::max(1u, std::thread::hardware_concurrency()), (unsigned)n);
+    if (nt <= 1) {
+        for (int k = 0; k < n; ++k) f(k);
+        return;
+    }
+    std::vector<std::thread> th;
+    for (int t = 0; t < nt; ++t)
+        th.emplace_back([&, t] {
+            for (int k = t; k < n; k += nt) f(k);
+        });
+    for (auto &x : th) x.join();
+}
+
+// ---- multiplicative perturbation construction (eqs. (8)-(11)) -------------
+
+// a_idx = b_r D^m, idx = r + m N (eq. (8)); Dpow[m + 1] = D^m for m >= -1.
+struct Sequence {
+    int N, c;
+    const std::vector<double> *B;
+    std::vector<std::vector<double>> Dpow;
+    void row(int idx, double *out) const {
+        int m = idx >= 0 ? idx / N : -((-idx + N - 1) / N);
+        int r = idx - m * N;
+        const std::vector<double> &P = Dpow[m + 1];
+        la::matmul(B->data() + (size_t)r * c, P.data(), out, 1, c, c);
+    }
+};
+
+bool make_sequence(const std::vector<double> &B, const std::vector<double> &D, int N, int c,
+                   int max_idx, Sequence &s) {
+    s.N = N;
+    s.c = c;
+    s.B = &B;
+    const int mmax = max_idx / N + 1;
+    s.Dpow.assign(mmax + 2, std::vector<double>((size_t)c * c, 0.0));
+    std::vector<double> Dinv = D;
+    if (!la::inverse(Dinv.data(), c)) return false;
+    s.Dpow[0] = Dinv;                                            // D^{-1}
+    for (int i = 0; i < c; ++i) s.Dpow[1][(size_t)i * c + i] = 1.0;   // D^0
+    for (int m = 1; m <= mmax; ++m) la::matmul(s.Dpow[m].data(), D.data(), s.Dpow[m + 1].data(), c, c, c);
+    return true;
+}
+
+// U_k = A_{N-1-k}^{-1} (eq. (10)), R_i[l,:] = a_{l-i} (eq. (11)).
+int mpc_plan(cerar_plan *p) {
+    const int N = p->N, c = p->c, L = p->L;
+    Sequence s;
+    if (!make_sequence(p->B, p->D, N, c, L + N, s))
+        return fail(CERAR_E_SINGULAR, "perturbation matrix D is singular");
+    p->U.assign((size_t)N * c * c, 0.0);
+    p->R.assign((size_t)N * (L + 1) * c, 0.0);
+    for (int k = 0; k < N; ++k) {
+        double *Uk = p->U.data() + (size_t)k * c * c;
+        const int ell = N - 1 - k;
+        for (int t = 0; t < c; ++t) s.row(ell + t, Uk + (size_t)t * c);
+        if (!la::inverse(Uk, c))
+            return fail(CERAR_E_SINGULAR, "window A_%d of the construction is singular", ell);
+    }
+    for (int i = 0; i < N; ++i)
+        for (int l = 0; l <= L; ++l) s.row(l - i, p->R.data() + ((size_t)i * (L + 1) + l) * c);
+    return CERAR_OK;
+}
+
+// ---- coefficient maps and Phi (eqs. (6), (7)) ------------------------------
+
+// Block r of M_i R_i is U_{i+r} W_{N-1-r}(R_i) (c x c).
+void block_product(const cerar_plan *p, const std::vector<double> &U, const std::vector<double> &R,
+                   int i, int r, double *out) {
+    const int N = p->N, c = p->c, L = p->L;
+    const double *Uk = U.data() + (size_t)((i + r) % N) * c * c;
+    const double *W = R.data() + ((size_t)i * (L + 1) + (N - 1 - r)) * c;
+    la::matmul(Uk, W, out, c, c, c);
+}
+
+double phi_of(const cerar_plan *p, const std::vector<double> &U, const std::vector<double> &R) {
+    const int N = p->N, c = p->c;
+    std::vector<double> blk((size_t)c * c);
+    double total = 0.0;
+    for (int i = 0; i < N; ++i)
+        for (int r = 0; r < N; ++r) {
+            block_product(p, U, R, i, r, blk.data());
+            for (int a = 0; a < c; ++a) blk[(size_t)a * c + a] -= 1.0;
+            total += la::frobenius2(blk.data(), blk.size());
+        }
+    return total;
+}
+
+std::vector<double> coefficient_map(const cerar_plan *p, const std::vector<double> &U, int i) {
+    const int N = p->N, c = p->c, L = p->L;
+    std::vector<double> M((size_t)N * c * (L + 1), 0.0);
+    for (int r = 0; r < N; ++r) {
+        const double *Uk = U.data() + (size_t)((i + r) % N) * c * c;
+        const int col0 = N - 1 - r;
+        for (int a = 0; a < c; ++a)
+            for (int b = 0; b < c; ++b) M[((size_t)r * c + a) * (L + 1) + col0 + b] = Uk[(size_t)a * c + b];
+    }
+    return M;
+}
+
+// ---- constrained design (Sec. II-D): U-step, R-step, projection -----------
+
+// U_k (sum_r W_r W_r^T) = sum_r W_r^T with W_r = W_{N-1-r}(R_{k-r}).
+bool u_step(const cerar_plan *p, const std::vector<double> &R, std::vector<double> &U) {
+    const int N = p->N, c = p->c, L = p->L;
+    bool ok = true;
+    std::mutex mu;
+    parallel_for(N, [&](int k) {
+        std::vector<double> gram((size_t)c * c, 0.0), rhsT((size_t)c * c, 0.0);
+        for (int r = 0; r < N; ++r) {
+            const int owner = ((k - r) % N + N) % N;
+            const double *W = R.data() + ((size_t)owner * (L + 1) + (N - 1 - r)) * c;
+            for (int a = 0; a < c; ++a)
+                for (int b = 0; b < c; ++b) {
+                    double s = 0.0;
+                    for (int t = 0; t < c; ++t) s += W[(size_t)a * c + t] * W[(size_t)b * c + t];
+                    gram[(size_t)a * c + b] += s;
+                }
+            for (int a = 0; a < c * c; ++a) rhsT[a] += W[a];      // (W^T)^T = W
+        }
+        // gram^T U_k^T = (sum W^T)^T = sum W ; gram is symmetric
+        if (!la::solve(gram.data(), c, rhsT.data(), c)) {
+            std::lock_guard<std::mutex> g(mu);
+            ok = false;
+            return;
+        }
+        double *Uk = U.data() + (size_t)k * c * c;
+        for (int a = 0; a < c; ++a)
+            for (int b = 0; b < c; ++b) Uk[(size_t)a * c + b] = rhsT[(size_t)b * c + a];
+    });
+    return ok;
+}
+
+// R_i = argmin ||M_i R - T||_F.
+bool r_step(const cerar_plan *p, const std::vector<double> &U, std::vector<double> &R) {
+    const int N = p->N, c = p->c, L = p->L;
+    std::vector<double> T((size_t)N * c * c, 0.0);
+    for (int r = 0; r < N; ++r)
+        for (int a = 0; a < c; ++a) T[((size_t)r * c + a) * c + a] = 1.0;
+    bool ok = true;
+    std::mutex mu;
+    parallel_for(N, [&](int i) {
+        std::vector<double> M = coefficient_map(p, U, i);
+        if (!la::lstsq(M.data(), N * c, L + 1, T.data(), c, R.data() + (size_t)i * (L + 1) * c)) {
+            std::lock_guard<std::mutex> g(mu);
+            ok = false;
+        }
+    });
+    return ok;
+}
+
+// Clip every U_k's singular values into [a0, b0], b0/a0 = kappa_max/sqrt(N),
+// geometrically centred on the geometric mean of all singular values.
+void project(const cerar_plan *p, std::vector<double> &U, double kappa_max, double &a0, double &b0) {
+    const int N = p->N, c = p->c;
+    std::vector<double> P((size_t)N * c * c), S((size_t)N * c), Q((size_t)N * c * c);
+    parallel_for(N, [&](int k) {
+        la::svd_square(U.data() + (size_t)k * c * c, c, P.data() + (size_t)k * c * c,
+                       S.data() + (size_t)k * c, Q.data() + (size_t)k * c * c);
+    });
+    double logsum = 0.0;
+    for (double s : S) logsum += std::log(s);
+    const double centre = std::exp(logsum / (double)S.size());
+    const double half = std::sqrt(kappa_max / std::sqrt((double)N));
+    a0 = centre / half;
+    b0 = centre * half;
+    for (int k = 0; k < N; ++k) {
+        const double *Pk = P.data() + (size_t)k * c * c, *Qk = Q.data() + (size_t)k * c * c;
+        const double *Sk = S.data() + (size_t)k * c;
+        double *Uk = U.data() + (size_t)k * c * c;
+        for (int a = 0; a < c; ++a)
+            for (int b = 0; b < c; ++b) {
+                double v = 0.0;
+                for (int t = 0; t < c; ++t)
+                    v += Pk[(size_t)a * c + t] * std::min(std::max(Sk[t], a0), b0) * Qk[(size_t)b * c + t];
+                Uk[(size_t)a * c + b] = v;
+            }
+    }
+}
+
+double kappa_of(const double *A, int m, int n) {
+    std::vector<double> s = la::singular_values(A, m, n);
+    return s.back() > 0 ? s.front() / s.back() : std::numeric_limits<double>::infinity();
+}
+
+void fill_info(cerar_plan *p, cerar_construction kind, double param) {
+    const int N = p->N, c = p->c, L = p->L;
+    cerar_plan_info &I = p->info;
+    I.N = N;
+    I.c = c;
+    I.L = L;
+    I.r_star = (c + N - 1) / N - 1;
+    I.kind = kind;
+    I.param = param;
+    I.comm_rate = (double)L / c;
+    I.storage_rate = 1.0 + (double)N / c;
+    I.phi = phi_of(p, p->U, p->R);
+    std::vector<double> kM(N), kU(N), kR(N), nU(N), nR(N);
+    parallel_for(N, [&](int i) {
+        std::vector<double> M = coefficient_map(p, p->U, i);
+        kM[i] = kappa_of(M.data(), N * c, L + 1);
+        std::vector<double> su = la::singular_values(p->U.data() + (size_t)i * c * c, c, c);
+        kU[i] = su.back() > 0 ? su.front() / su.back() : INFINITY;
+        nU[i] = su.front();
+        std::vector<double> sr = la::singular_values(p->R.data() + (size_t)i * (L + 1) * c, L + 1, c);
+        kR[i] = sr.back() > 0 ? sr.front() / sr.back() : INFINITY;
+        nR[i] = sr.front();
+    });
+    I.kappa_M = *std::max_element(kM.begin(), kM.end());
+    I.kappa_U = *std::max_element(kU.begin(), kU.end());
+    I.kappa_R = *std::max_element(kR.begin(), kR.end());
+    I.amplification = *std::max_element(nU.begin(), nU.end()) * *std::max_element(nR.begin(), nR.end());
+    I.fp64_reliable = (I.kappa_U * c * 0x1.0p-53 <= 1e-6) ? 1 : 0;
+    if (!p->D.empty()) {
+        std::vector<double> E = p->D;
+        if (la::inverse(E.data(), c)) {
+            for (int a = 0; a < c; ++a) E[(size_t)a * c + a] -= 1.0;
+            I.phi_closed_form = N * (N - 1) / 2.0 * la::frobenius2(E.data(), E.size());
+        } else {
+            I.phi_closed_form = kNaN;
+        }
+    } else {
+        I.phi_closed_form = kNaN;
+    }
+}
+
+int validate(const cerar_plan_desc *d) {
+    if (!d) return fail(CERAR_E_INVAL, "desc is NULL");
+    if (d->N < 2 || d->N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [2, %d] (Algorithm 1 needs N >= 2)", d->N, kMaxN);
+    if (d->c < d->N || d->c > kMaxC) return fail(CERAR_E_INVAL, "c=%d outside [N=%d, %d]", d->c, d->N, kMaxC);
+    if (!std::isfinite(d->param)) return fail(CERAR_E_INVAL, "param is not finite");
+    switch (d->kind) {
+        case CERAR_VANDERMONDE:
+            if (d->param <= 0) return fail(CERAR_E_INVAL, "Vandermonde tau=%g must be > 0", d->param);
+            break;
+        case CERAR_O_EPS:
+            if (d->param < 0) return fail(CERAR_E_INVAL, "eps=%g must be >= 0", d->param);
+            break;
+        case CERAR_KAPPA:
+            if (d->param < std::sqrt((double)d->N))
+                return fail(CERAR_E_INVAL, "kappa_max=%g below sqrt(N)=%g: the projection interval would be empty",
+                            d->param, std::sqrt((double)d->N));
+            break;
+        default:
+            return fail(CERAR_E_INVAL, "unknown construction %d", (int)d->kind);
+    }
+    return CERAR_OK;
+}
+
+}  // namespace
+
+std::string build_ring_tables(int N, int c, RingTables &t) {
+    const int L = c + N - 2;
+    t.N = N;
+    t.c = c;
+    t.L = L;
+    t.enc_copy.assign(N, -1);
+    t.rounds.assign((size_t)(L + 1) * N, RoundOp{-1, -1, -1, -1});
+    t.state.assign((size_t)(L + 1) * N * (c + N), -1);
+    std::vector<std::vector<int>> D(N, std::vector<int>(c)), Bs(N, std::vector<int>(N - 1, -1));
+    std::vector<int> X(N, -1), next_pool(N, 0);
+    auto pool = [&](int i) { return N * c + i * N + next_pool[i]++; };
+    auto snapshot = [&](int k) {
+        for (int i = 0; i < N; ++i) {
+            int *s = t.state.data() + ((size_t)k * N + i) * (c + N);
+            for (int j = 0; j < c; ++j) s[j] = D[i][j];
+            for (int j = 0; j < N - 1; ++j) s[c + j] = Bs[i][j];
+            s[c + N - 1] = X[i];
+        }
+    };
+    for (int i = 0; i < N; ++i) {
+        for (int j = 0; j < c; ++j) D[i][j] = i * c + j;     // delta_{i,j+1}, encoded in place
+        X[i] = pool(i);                                      // x_{i,1} = delta_{i,1}, a copy
+        t.enc_copy[i] = X[i];
+    }
+    snapshot(0);
+    for (int k = 1; k <= L; ++k) {
+        std::vector<int> recv(N);
+        for (int i = 0; i < N; ++i) recv[i] = X[(i - 1 + N) % N];   // handoff W_{i-1} -> W_i
+        for (int i = 0; i < N; ++i) {
+            RoundOp &op = t.rounds[(size_t)k * N + i];
+            if (k <= N - 1) {
+                Bs[i][k - 1] = recv[i];                      // B_{i,k} <- x_{i-1,k}
+                const int s = pool(i);
+                op = RoundOp{recv[i], -1, D[i][k], s};       // x_{i,k+1} = x_{i-1,k} + delta_{i,k+1}
+                X[i] = s;
+            } else {
+                const int j = k - N + 1;                     // 1-based
+                const int old = D[i][j - 1];
+                D[i][j - 1] = recv[i];                       // D_{i,j} <- x_{i-1,k}
+                if (k < L) {
+                    const int add = (k + 1 <= c) ? D[i][k] : -1;
+                    op = RoundOp{recv[i], old, add, old};    // x_{i,k+1} = sigma_{i,k} (+ delta_{i,k+1})
+                    X[i] = old;
+                } else {
+                    X[i] = -1;                               // round L only stores
+                }
+            }
+        }
+        snapshot(k);
+    }
+    t.ycols.assign((size_t)N * (L + 1), -1);
+    for (int i = 0; i < N; ++i) {
+        for (int j = 0; j < N - 1; ++j) t.ycols[(size_t)i * (L + 1) + j] = Bs[i][j];
+        for (int j = 0; j < c; ++j) t.ycols[(size_t)i * (L + 1) + N - 1 + j] = D[i][j];
+    }
+    // Hazard check per launch: a written slot is read by nobody else, and
+    // written once; every slot id is in range.
+    const int nslots = N * c + N * N;
+    for (int k = 1; k <= L; ++k) {
+        std::map<int, int> writer;
+        for (int i = 0; i < N; ++i) {
+            const RoundOp &op = t.rounds[(size_t)k * N + i];
+            if (op.dst < 0) continue;
+            if (op.dst >= nslots) return "slot out of range";
+            if (writer.count(op.dst)) return "slot written twice in one round";
+            writer[op.dst] = i;
+        }
+        for (int i = 0; i < N; ++i) {
+            const RoundOp &op = t.rounds[(size_t)k * N + i];
+            if (op.dst < 0) continue;
+            for (int s : {op.recv, op.sub, op.add}) {
+                if (s < 0) continue;
+                if (s >= nslots) return "slot out of range";
+                auto it = writer.find(s);
+                if (it != writer.end() && !(it->second == i && s == op.dst && s == op.sub))
+                    return "round reads a slot another operand writes";
+            }
+        }
+    }
+    std::set<int> seen;
+    for (int s : t.ycols) {
+        if (s < 0 || s >= nslots) return "observation slot out of range";
+        if (!seen.insert(s).second) return "two observations share a slot";
+    }
+    return "";
+}
+
+void build_fragments(cerar_plan *p) {
+    const int N = p->N, c = p->c, L = p->L;
+    p->MT = ceil_div(c, kTileM);
+    p->KSe = ceil_div(c, kTileK);
+    p->KSd = ceil_div(L + 1, kTileK);
+    // A operand of a 16x16x4 fp32 MFMA: lane l holds A[row = l % 16][k = l / 16].
+    // Encode computes delta^T = U^T G^T: row = output chunk j, k = input chunk l.
+    p->enc_frag.assign((size_t)N * p->MT * p->KSe * kLanes, 0.0f);
+    for (int i = 0; i < N; ++i)
+        for (int mt = 0; mt < p->MT; ++mt)
+            for (int ks = 0; ks < p->KSe; ++ks)
+                for (int lane = 0; lane < kLanes; ++lane) {
+                    const int j = mt * kTileM + lane % kTileM, l = ks * kTileK + lane / kTileM;
+                    float v = 0.0f;
+                    if (j < c && l < c) v = (float)p->U[((size_t)i * c + l) * c + j];
+                    p->enc_frag[(((size_t)i * p->MT + mt) * p->KSe + ks) * kLanes + lane] = v;
+                }
+    // Decode computes g_hat^T = R^T Y^T: row = output chunk m, k = observation.
+    p->dec_frag.assign((size_t)N * p->MT * p->KSd * kLanes, 0.0f);
+    for (int i = 0; i < N; ++i)
+        for (int mt = 0; mt < p->MT; ++mt)
+            for (int ks = 0; ks < p->KSd; ++ks)
+                for (int lane = 0; lane < kLanes; ++lane) {
+                    const int m = mt * kTileM + lane % kTileM, k = ks * kTileK + lane / kTileM;
+                    float v = 0.0f;
+                    if (m < c && k <= L) v = (float)p->R[((size_t)i * (L + 1) + k) * c + m];
+                    p->dec_frag[(((size_t)i * p->MT + mt) * p->KSd + ks) * kLanes + lane] = v;
+                }
+}
+
+}  // namespace cerar
+
+using namespace cerar;
+
+static int finish_plan(cerar_plan *p, cerar_construction kind, double param, cerar_plan **out) {
+    std::string err = build_ring_tables(p->N, p->c, p->tab);
+    if (!err.empty()) return fail(CERAR_E_INVAL, "ownership table: %s", err.c_str());
+    for (double v : p->U)
+        if (!std::isfinite(v)) return fail(CERAR_E_SINGULAR, "encoding matrix has non-finite entries");
+    for (double v : p->R)
+        if (!std::isfinite(v)) return fail(CERAR_E_SINGULAR, "decoding matrix has non-finite entries");
+    fill_info(p, kind, param);
+    build_fragments(p);
+    *out = p;
+    return CERAR_OK;
+}
+
+extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
+    clear_error();
+    if (!out) return fail(CERAR_E_INVAL, "out is NULL");
+    *out = nullptr;
+    int st = validate(desc);
+    if (st) return st;
+    const int N = desc->N, c = desc->c;
+    std::vector<double> nodes = desc->nodes ? std::vector<double>(desc->nodes, desc->nodes + c) : chebyshev_nodes(c);
+    {
+        std::vector<double> sorted = nodes;
+        std::sort(sorted.begin(), sorted.end());
+        for (int j = 0; j < c; ++j)
+            if (!std::isfinite(sorted[j]) || (j > 0 && sorted[j] == sorted[j - 1]))
+                return fail(CERAR_E_INVAL, "Vandermonde nodes must be distinct finite reals");
+    }
+    std::vector<double> H((size_t)c * c, 0.0);
+    if (desc->perturb) {
+        H.assign(desc->perturb, desc->perturb + (size_t)c * c);
+    } else {
+        for (int j = 0; j < c; ++j) H[(size_t)j * c + j] = nodes[j];
+    }
+    cerar_plan *p = new (std::nothrow) cerar_plan();
+    if (!p) return fail(CERAR_E_NOMEM, "out of host memory");
+    p->N = N;
+    p->c = c;
+    p->L = c + N - 2;
+    p->info.phi_initial = kNaN;
+    p->info.proj_a0 = p->info.proj_b0 = kNaN;
+    int result = CERAR_OK;
+    if (desc->kind == CERAR_VANDERMONDE) {
+        // z_j = exp(tau xi_j); b_l = [z_j^l], l < N; D = diag(z_j^N)
+        p->B.assign((size_t)N * c, 0.0);
+        p->D.assign((size_t)c * c, 0.0);
+        for (int j = 0; j < c; ++j) {
+            const double z = std::exp(desc->param * nodes[j]);
+            for (int l = 0; l < N; ++l) p->B[(size_t)l * c + j] = std::pow(z, (double)l);
+            p->D[(size_t)j * c + j] = std::pow(z, (double)N);
+        }
+        result = mpc_plan(p);
+    } else {
+        const double eps = desc->kind == CERAR_O_EPS ? desc->param : (desc->eps0 > 0 ? desc->eps0 : 0.3);
+        if (desc->kind == CERAR_O_EPS && eps > 0) {
+            std::vector<double> s = la::singular_values(H.data(), c, c);
+            if (eps * s.front() >= 1.0) {
+                delete p;
+                return fail(CERAR_E_INVAL, "eps ||H||_2 = %g must be < 1 (Sec. II-C)", eps * s.front());
+            }
+        }
+        p->D.assign((size_t)c * c, 0.0);
+        for (size_t a = 0; a < H.size(); ++a) p->D[a] = eps * H[a];
+        for (int j = 0; j < c; ++j) p->D[(size_t)j * c + j] += 1.0;
+        const int tries = desc->base ? 1 : 8;
+        for (int t = 0; t < tries; ++t) {
+            if (desc->base) {
+                p->B.assign(desc->base, desc->base + (size_t)N * c);
+                p->info.seed_used = 0;
+            } else {
+                p->B = gaussian_base(desc->seed + (uint64_t)t, N, c);
+                p->info.seed_used = desc->seed + (uint64_t)t;
+            }
+            result = mpc_plan(p);
+            if (result != CERAR_E_SINGULAR) break;
+        }
+        if (result == CERAR_OK && desc->kind == CERAR_KAPPA) {
+            p->info.phi_initial = phi_of(p, p->U, p->R);
+            const int iters = desc->als_iters > 0 ? desc->als_iters : 100;
+            double a0 = kNaN, b0 = kNaN;
+            for (int it = 0; it < iters && result == CERAR_OK; ++it) {
+                if (!u_step(p, p->R, p->U)) result = fail(CERAR_E_SINGULAR, "U-step normal equations singular");
+                else if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
+                else project(p, p->U, desc->param, a0, b0);
+            }
+            if (result == CERAR_OK && !r_step(p, p->U, p->R))
+                result = fail(CERAR_E_SINGULAR, "final R-step rank deficient");
+            p->info.proj_a0 = a0;
+            p->info.proj_b0 = b0;
+            p->D.clear();                                  // no closed form for the designed plan
+        }
+    }
+    if (result == CERAR_OK) result = finish_plan(p, desc->kind, desc->param, out);
+    if (result != CERAR_OK) delete p;
+    return result;
+}
+
+extern "C" int cerar_plan_create(int N, int c, cerar_construction kind, double param, uint64_t seed,
+                                 cerar_plan **out) {
+    cerar_plan_desc d;
+    std::memset(&d, 0, sizeof d);
+    d.N = N;
+    d.c = c;
+    d.kind = kind;
+    d.param = param;
+    d.seed = seed;
+    return cerar_plan_create_desc(&d, out);
+}
+
+extern "C" int cerar_plan_create_explicit(int N, int c, const double *U, const double *R, cerar_plan **out) {
+    clear_error();
+    if (!out) return fail(CERAR_E_INVAL, "out is NULL");
+    *out = nullptr;
+    if (!U || !R) return fail(CERAR_E_INVAL, "U and R must be non-NULL");
+    if (N < 2 || N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [2, %d]", N, kMaxN);
+    if (c < N || c > kMaxC) return fail(CERAR_E_INVAL, "c=%d outside [N=%d, %d]", c, N, kMaxC);
+    cerar_plan *p = new (std::nothrow) cerar_plan();
+    if (!p) return fail(CERAR_E_NOMEM, "out of host memory");
+    p->N = N;
+    p->c = c;
+    p->L = c + N - 2;
+    p->U.assign(U, U + (size_t)N * c * c);
+    p->R.assign(R, R + (size_t)N * (p->L + 1) * c);
+    p->info.phi_initial = kNaN;
+    p->info.proj_a0 = p->info.proj_b0 = kNaN;
+    int result = finish_plan(p, CERAR_EXPLICIT, kNaN, out);
+    if (result != CERAR_OK) delete p;
+    return result;
+}
+
+extern "C" void cerar_plan_destroy(cerar_plan *plan) {
+    if (!plan) return;
+    release_device(plan);
+    delete plan;
+}
+
+extern "C" int cerar_plan_get_info(const cerar_plan *plan, cerar_plan_info *info) {
+    clear_error();
+    if (!plan || !info) return fail(CERAR_E_INVAL, "plan and info must be non-NULL");
+    *info = plan->info;
+    return CERAR_OK;
+}
+
+extern "C" int cerar_plan_get_matrices(const cerar_plan *plan, double *U, double *R) {
+    clear_error();
+    if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
+    if (U) std::copy(plan->U.begin(), plan->U.end(), U);
+    if (R) std::copy(plan->R.begin(), plan->R.end(), R);
+    return CERAR_OK;
+}
+
+extern "C" int cerar_chunk_len(const cerar_plan *plan, size_t d, size_t *p, size_t *pool_stride) {
+    clear_error();
+    if (!plan || !p || !pool_stride) return fail(CERAR_E_INVAL, "NULL argument");
+    if (d == 0) return fail(CERAR_E_INVAL, "d must be > 0");
+    *p = (d + plan->c - 1) / plan->c;
+    *pool_stride = (*p + 63) / 64 * 64;
+    return CERAR_OK;
+}
+
+extern "C" int cerar_workspace_bytes(const cerar_plan *plan, size_t d, size_t *bytes) {
+    size_t p, stride;
+    int st = cerar_chunk_len(plan, d, &p, &stride);
+    if (st) return st;
+    if (!bytes) return fail(CERAR_E_INVAL, "bytes is NULL");
+    *bytes = (size_t)plan->tab.pool_slots() * stride * sizeof(float);
+    return CERAR_OK;
+}
+
+extern "C" int cerar_slot_map(const cerar_plan *plan, int step, int *slots) {
+    clear_error();
+    if (!plan || !slots) return fail(CERAR_E_INVAL, "NULL argument");
+    if (step < 0 || step > plan->L) return fail(CERAR_E_INVAL, "step %d outside [0, L=%d]", step, plan->L);
+    const size_t n = (size_t)plan->N * (plan->c + plan->N);
+    std::copy(plan->tab.state.begin() + (size_t)step * n, plan->tab.state.begin() + (size_t)(step + 1) * n, slots);
+    return CERAR_OK;
+}
+
+extern "C" const char *cerar_last_error(void) { return cerar::g_last_error.c_str(); }

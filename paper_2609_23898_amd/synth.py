@@ -238,28 +238,34 @@ class Workload:
         v = (n * s).astype(np.float32)
         return np.where(valid, v, np.float32(0.0))
 
+    def values_torch(self, worker, idx):
+        """Same values as ``values_np`` for an int64 torch tensor of flat
+        indices, on the tensor's device."""
+        import torch
+        dev = idx.device
+        key = self.worker_key(worker)
+        offsets = torch.as_tensor(self._offsets, device=dev)
+        scales = torch.as_tensor(self._scales.astype(np.float64), device=dev)
+        valid = idx < self.d
+        idx_c = torch.where(valid, idx, torch.zeros_like(idx))
+        n = normal_torch(key, idx_c)
+        if self.outlier_prob > 0:
+            hit = uniform32_torch(key, idx_c, 6) < self.outlier_threshold
+            n = torch.where(hit, n * float(self.outlier_factor), n)
+        t = torch.searchsorted(offsets, idx_c, right=True) - 1
+        v = (n * scales[t]).to(torch.float32)
+        return torch.where(valid, v, torch.zeros_like(v))
+
     def fill_torch(self, out, worker, start=0, chunk=1 << 24):
         """Write entries [start, start + out.numel()) of ``worker`` into the
         float32 tensor ``out`` (any device), chunk by chunk."""
         import torch
-        dev = out.device
-        count = out.numel()
-        key = self.worker_key(worker)
-        offsets = torch.as_tensor(self._offsets, device=dev)
-        scales = torch.as_tensor(self._scales.astype(np.float64), device=dev)
         flat = out.view(-1)
+        count = flat.numel()
         for lo in range(0, count, chunk):
             hi = min(count, lo + chunk)
-            idx = torch.arange(start + lo, start + hi, dtype=torch.int64, device=dev)
-            valid = idx < self.d
-            idx_c = torch.where(valid, idx, torch.zeros_like(idx))
-            n = normal_torch(key, idx_c)
-            if self.outlier_prob > 0:
-                hit = uniform32_torch(key, idx_c, 6) < self.outlier_threshold
-                n = torch.where(hit, n * float(self.outlier_factor), n)
-            t = torch.searchsorted(offsets, idx_c, right=True) - 1
-            v = (n * scales[t]).to(torch.float32)
-            flat[lo:hi] = torch.where(valid, v, torch.zeros_like(v))
+            idx = torch.arange(start + lo, start + hi, dtype=torch.int64, device=out.device)
+            flat[lo:hi] = self.values_torch(worker, idx)
         return out
 
 

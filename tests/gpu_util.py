@@ -1,0 +1,100 @@
+"""Shared helpers of the GPU parity tests: device buffers, slot reads, and the
+oracle run on the same seeded inputs."""
+
+import numpy as np
+
+from oracle import plan as OP
+from oracle import ring as OR
+from paper_2609_23898_amd import cerar as C
+from paper_2609_23898_amd import synth
+
+U32 = 2.0 ** -24
+
+
+def torch_dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    return torch, "cuda:0"
+
+
+def host_grads(N, d, seed, scale=1.0, outlier_prob=0.0):
+    w = synth.Workload("test", N, N, d, seed=seed, scale=scale, outlier_prob=outlier_prob,
+                       outlier_factor=100.0)
+    return np.stack([w.values_np(i, np.arange(d)) for i in range(N)])
+
+
+def to_device(a, ld=None, align_elems=0):
+    """(N, d) float32 array -> (N, ld) device tensor view (row stride ld)."""
+    torch, dev = torch_dev()
+    N, d = a.shape
+    ld = ld or d
+    buf = torch.zeros(N * ld + align_elems, dtype=torch.float32, device=dev)
+    t = buf[align_elems:].view(N, ld)
+    t[:, :d] = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    return t
+
+
+def buffers(plan, d, ld_work=None, ld_out=None, work_offset=0, out_offset=0, ws_offset=0):
+    torch, dev = torch_dev()
+    p, stride = plan.chunk_len(d)
+    ld_work = ld_work or plan.c * p
+    ld_out = ld_out or d
+    work = torch.full((plan.N * ld_work + work_offset,), float("nan"), dtype=torch.float32,
+                      device=dev)[work_offset:].view(plan.N, ld_work)
+    nbytes = plan.workspace_bytes(d)
+    ws = torch.zeros(nbytes + 4 * ws_offset, dtype=torch.uint8, device=dev)[4 * ws_offset:]
+    out = torch.full((plan.N * ld_out + out_offset,), float("nan"), dtype=torch.float32,
+                     device=dev)[out_offset:].view(plan.N, ld_out)
+    return work, ws, out
+
+
+def read_slot(plan, d, work, ws, s):
+    """Host copy of the p floats of slot s."""
+    torch, _ = torch_dev()
+    p, stride = plan.chunk_len(d)
+    Nc = plan.N * plan.c
+    if s < Nc:
+        w, l = divmod(s, plan.c)
+        return work[w, l * p:(l + 1) * p].double().cpu().numpy()
+    wsf = ws.view(torch.float32)
+    q = s - Nc
+    return wsf[q * stride:q * stride + p].double().cpu().numpy()
+
+
+def oracle_allreduce(grads, U, R):
+    return OR.allreduce(grads, U, R)
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / nb) if nb > 0 else float(np.linalg.norm(a - b))
+
+
+def max_rel_l2(gpu, ref):
+    return max(rel_l2(gpu[i], ref[i]) for i in range(len(ref)))
+
+
+def orthogonal_plan(N, c, seed):
+    """A well-conditioned explicit plan: random orthogonal U_k and the
+    least-squares decoders R_i for them (oracle r_step)."""
+    rng = np.random.default_rng(seed)
+    U = np.stack([np.linalg.qr(rng.standard_normal((c, c)))[0] for _ in range(N)])
+    R = OP.r_step(U)
+    return U, R
+
+
+def mpc_plan(N, c, eps, seed):
+    B = synth.base_matrix(seed, N, c)
+    D = OP.o_eps_perturbation(np.diag(OP.chebyshev_nodes(c)), eps)
+    return OP.mpc_plan(B, D)
+
+
+def gate(kappa_M):
+    """Parity bar: relative l2 <= 1e-4 for plans with kappa_2(M) <= 1e3;
+    larger condition numbers are reported against a looser bound that grows
+    with kappa (fp32 rounding amplified by the decode)."""
+    if kappa_M <= 1e3:
+        return 1e-4
+    return max(1e-4, 64 * kappa_M * U32)

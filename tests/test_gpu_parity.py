@@ -1,0 +1,289 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle on the same
+seeded inputs: each kernel step, the per-round buffer state, and the whole
+all-reduce, over vector and scalar layouts, ragged tails, in-place encode,
+N = 2 and c = N edge cases, error norms, buckets and the copy kernel."""
+
+import numpy as np
+import pytest
+
+from oracle import plan as OP
+from oracle import ring as OR
+from paper_2609_23898_amd import cerar as C
+
+from gpu_util import (U32, buffers, gate, host_grads, max_rel_l2, mpc_plan, orthogonal_plan, read_slot,
+                      rel_l2, to_device, torch_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def sync():
+    torch, _ = torch_dev()
+    torch.cuda.synchronize()
+
+
+# --- K1 encode -------------------------------------------------------------------
+
+@pytest.mark.parametrize("N,c,d", [(4, 4, 4096), (3, 7, 1001), (8, 16, 16 * 777), (2, 64, 64 * 300 + 5),
+                                   (4, 128, 128 * 64 + 3)])
+def test_encode_with_permutations_is_exact(N, c, d):
+    """U_k = permutation matrices: every delta is one input chunk, so the MFMA
+    tiles must reproduce the inputs bit for bit (checks the lane layout)."""
+    rng = np.random.default_rng(c)
+    U = np.stack([np.eye(c)[rng.permutation(c)] for _ in range(N)])
+    R = np.zeros((N, c + N - 1, c))
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=1)
+    grads = to_device(g)
+    work, ws, _ = buffers(plan, d)
+    C.encode_round(plan, 0, d, grads, work, ws)
+    sync()
+    p, _ = plan.chunk_len(d)
+    for i in range(N):
+        G = OR.to_chunks(g[i], c).astype(np.float32)
+        expect = G @ U[i].astype(np.float32)
+        got = work[i, :c * p].cpu().numpy().reshape(c, p).T
+        np.testing.assert_array_equal(got, expect)
+        x1 = read_slot(plan, d, work, ws, plan.slot_map(0)[i, c + N - 1])
+        np.testing.assert_array_equal(x1, expect[:, 0])
+
+
+@pytest.mark.parametrize("N,c,d,misalign", [(4, 4, 4096, 0), (3, 7, 1001, 0), (8, 64, 64 * 500 + 7, 0),
+                                            (8, 16, 16 * 1024, 1), (2, 128, 128 * 70, 0), (5, 9, 9 * 64, 0)])
+def test_encode_matches_oracle_within_dot_product_bound(N, c, d, misalign):
+    """|delta_gpu - delta| <= (c + 4) u32 (|G| |U|) elementwise: fp32-rounded
+    coefficients, fp32 products and any summation order fit this bound."""
+    U, R = orthogonal_plan(N, c, seed=N + c)
+    U = U * np.random.default_rng(1).uniform(0.5, 2.0, size=(N, 1, c))   # not orthogonal any more
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=2)
+    grads = to_device(g, align_elems=misalign)
+    work, ws, _ = buffers(plan, d, work_offset=misalign)
+    C.encode_round(plan, 0, d, grads, work, ws)
+    sync()
+    p, _ = plan.chunk_len(d)
+    for i in range(N):
+        G = OR.to_chunks(g[i], c)
+        exact = OR.encode(G, U[i])
+        bound = (c + 4) * U32 * (np.abs(G) @ np.abs(U[i])) + 1e-38
+        got = work[i, :c * p].double().cpu().numpy().reshape(c, p).T
+        assert np.all(np.abs(got - exact) <= bound)
+
+
+# --- K2/K3 rounds: per-round buffer state ---------------------------------------------
+
+@pytest.mark.parametrize("N,c,d", [(4, 5, 5 * 300), (2, 2, 2 * 64), (3, 3, 3 * 101), (8, 16, 16 * 256 + 3),
+                                   (4, 9, 9 * 128)])
+def test_each_round_matches_algorithm1_state(N, c, d):
+    """After step k, the slots the ownership table names for D_{i,j}, B_{i,j}
+    and the next message x_{i,k+1} hold the oracle's Algorithm 1 values."""
+    U, R = orthogonal_plan(N, c, seed=3)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=3)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    Delta = [OR.encode(OR.to_chunks(g[i], c), U[i]) for i in range(N)]
+    trace = []
+    Y, _ = OR.run_protocol(Delta, trace=trace)
+    L = c + N - 2
+    for k in range(0, L + 1):
+        C.encode_round(plan, k, d, grads, work, ws)
+        sync()
+        sm = plan.slot_map(k)
+        for i in range(N):
+            for j in range(c):
+                ref = Delta[i][:, j] if k == 0 else trace[k - 1]["D"][i][j]
+                assert rel_l2(read_slot(plan, d, work, ws, sm[i, j]), ref) < 1e-5, (k, i, j)
+            for j in range(min(k, N - 1)):
+                ref = trace[k - 1]["B"][i][j]
+                assert rel_l2(read_slot(plan, d, work, ws, sm[i, c + j]), ref) < 1e-5, (k, i, "B", j)
+            if k < L:
+                ref = trace[k]["x"][i]                                   # x_{i,k+1}
+                assert rel_l2(read_slot(plan, d, work, ws, sm[i, c + N - 1]), ref) < 1e-5, (k, i, "x")
+    C.decode(plan, d, work, ws, out)
+    sync()
+    ref = np.stack([OR.from_chunks(OR.decode(Y[i], R[i]), d) for i in range(N)])
+    assert max_rel_l2(out.double().cpu().numpy(), ref) < 1e-5
+
+
+# --- whole ring: gate ---------------------------------------------------------------
+
+CASES = [
+    # name, N, c, d, plan kind, param
+    ("cfg1-vandermonde", 4, 4, 4096, "vandermonde", 0.5),
+    ("cfg1-o_eps", 4, 4, 4096, "o_eps", 1e-3),
+    ("cfg1-exact", 4, 4, 4096, "o_eps", 0.0),
+    ("N2-c5-ragged", 2, 5, 5 * 333 + 2, "o_eps", 0.2),
+    ("N3-c7-odd-p", 3, 7, 7 * 101 + 3, "o_eps", 0.3),
+    ("N8-c16-tail", 8, 16, 16 * 4096 + 9, "o_eps", 0.3),
+    ("N8-c32", 8, 32, 32 * 2048, "kappa", 1e3),
+    ("N8-c64-ragged", 8, 64, 64 * 1536 + 61, "kappa", 1e3),
+    ("N16-c128", 16, 128, 128 * 320, "kappa", 1e3),
+]
+
+
+def case_plan(N, c, kind, param):
+    if kind == "vandermonde":
+        B, D = OP.vandermonde_base(N, param, OP.chebyshev_nodes(c))
+        return OP.mpc_plan(B, D)
+    if kind == "o_eps":
+        return mpc_plan(N, c, param, seed=N * 1000 + c)
+    from paper_2609_23898_amd import synth
+    B = synth.base_matrix(N * 1000 + c, N, c)
+    return OP.kappa_design(B, np.diag(OP.chebyshev_nodes(c)), 0.3, param, 20 if c <= 64 else 4)
+
+
+@pytest.mark.parametrize("name,N,c,d,kind,param", CASES, ids=[x[0] for x in CASES])
+def test_ring_simulate_parity(name, N, c, d, kind, param):
+    U, R = case_plan(N, c, kind, param)
+    kappa = OP.max_kappa_M(U)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=N + c)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    sync()
+    gpu = out.double().cpu().numpy()
+    ref = OR.allreduce(g, U, R)
+    S = OR.exact_sum(g)
+    parity = max_rel_l2(gpu, ref)
+    err_gpu = max(rel_l2(gpu[i], S) for i in range(N))
+    err_orc = max(rel_l2(ref[i], S) for i in range(N))
+    print(f"{name}: kappa_M={kappa:.3g} parity={parity:.3g} err_gpu={err_gpu:.4g} err_oracle={err_orc:.4g}")
+    assert np.all(np.isfinite(gpu))
+    assert parity <= gate(kappa)
+    if kappa <= 1e3:
+        assert abs(err_gpu - err_orc) <= 1e-4
+    if kind == "o_eps" and param == 0.0:
+        assert err_orc < 1e-12 and err_gpu < 1e-5        # exact ring all-reduce (c = N)
+
+
+def test_in_place_encode_matches_out_of_place():
+    N, c, d = 4, 16, 16 * 1000
+    U, R = mpc_plan(N, c, 0.3, seed=9)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=9)
+    p, _ = plan.chunk_len(d)
+    torch, dev = torch_dev()
+    a = to_device(np.pad(g, ((0, 0), (0, c * p - d))), ld=c * p)   # grads with room for c*p
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, a, work, ws, out)
+    ws2 = torch.zeros_like(ws)
+    out2 = torch.empty_like(out)
+    C.ring_simulate(plan, d, a, a, ws2, out2)                        # encode in place
+    sync()
+    np.testing.assert_array_equal(out.cpu().numpy(), out2.cpu().numpy())
+
+
+def test_scalar_layout_matches_vector_layout():
+    """Misaligned strides force the scalar kernels; same values as vector ones."""
+    N, c, d = 4, 8, 8 * 512
+    U, R = mpc_plan(N, c, 0.3, seed=10)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=10)
+    p, _ = plan.chunk_len(d)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, to_device(g), work, ws, out)
+    work2, ws2, out2 = buffers(plan, d, ld_work=c * p + 1, ld_out=d + 3, out_offset=1)
+    C.ring_simulate(plan, d, to_device(g, ld=d + 1), work2, ws2, out2)
+    sync()
+    a, b = out.double().cpu().numpy(), out2[:, :d].double().cpu().numpy()
+    assert max_rel_l2(b, a) < 1e-6
+    ref = OR.allreduce(g, U, R)
+    assert max_rel_l2(b, ref) < 1e-4
+
+
+def test_decode_never_writes_beyond_d():
+    N, c, d = 3, 5, 5 * 64 + 2
+    U, R = mpc_plan(N, c, 0.3, seed=11)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=11)
+    work, ws, out = buffers(plan, d, ld_out=d + 64)
+    C.ring_simulate(plan, d, to_device(g), work, ws, out)
+    sync()
+    o = out.cpu().numpy()
+    assert np.all(np.isnan(o[:, d:]))
+    assert np.all(np.isfinite(o[:, :d]))
+
+
+def test_rerun_on_same_buffers_is_deterministic():
+    N, c, d = 8, 32, 32 * 999
+    U, R = mpc_plan(N, c, 0.3, seed=12)
+    plan = C.Plan.explicit(U, R)
+    grads = to_device(host_grads(N, d, seed=12))
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    first = out.clone()
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    sync()
+    assert bool((first == out).all())
+
+
+def test_step_order_enforced_on_device_buffers():
+    N, c, d = 4, 5, 500
+    U, R = mpc_plan(N, c, 0.3, seed=13)
+    plan = C.Plan.explicit(U, R)
+    grads = to_device(host_grads(N, d, seed=13))
+    work, ws, out = buffers(plan, d)
+    C.encode_round(plan, 0, d, grads, work, ws)
+    with pytest.raises(C.CerarError) as ei:
+        C.encode_round(plan, 2, d, grads, work, ws)
+    assert ei.value.status == -6
+    with pytest.raises(C.CerarError):
+        C.decode(plan, d, work, ws, out)
+    for k in range(1, c + N - 1):
+        C.encode_round(plan, k, d, grads, work, ws)
+    C.decode(plan, d, work, ws, out)
+    sync()
+
+
+# --- K5 error norms, buckets, copy -------------------------------------------------------
+
+def test_error_norms_kernel():
+    torch, dev = torch_dev()
+    N, d = 5, 100_003
+    g = host_grads(N, d, seed=14)
+    o = host_grads(N, d, seed=15)
+    norms = torch.empty(N + 1, dtype=torch.float64, device=dev)
+    C.error_norms(N, d, to_device(g), to_device(o), norms)
+    sync()
+    S = OR.exact_sum(g)
+    ref = [np.sum((o[i].astype(np.float64) - S) ** 2) for i in range(N)] + [np.sum(S * S)]
+    np.testing.assert_allclose(norms.cpu().numpy(), ref, rtol=1e-12)
+    N = 17
+    g = host_grads(N, 4097, seed=16)
+    norms = torch.empty(N + 1, dtype=torch.float64, device=dev)
+    C.error_norms(N, 4097, to_device(g), to_device(g), norms)
+    sync()
+    S = OR.exact_sum(g)
+    ref = [np.sum((g[i].astype(np.float64) - S) ** 2) for i in range(N)] + [np.sum(S * S)]
+    np.testing.assert_allclose(norms.cpu().numpy(), ref, rtol=1e-12)
+
+
+def test_bucketed_matches_independent_instances():
+    torch, dev = torch_dev()
+    N, c = 4, 8
+    buckets = [(0, 8 * 300), (8 * 300, 1001), (8 * 300 + 1001, 8 * 64), (8 * 364 + 1001, 13)]
+    d = buckets[-1][0] + buckets[-1][1]
+    U, R = mpc_plan(N, c, 0.3, seed=17)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=17)
+    work_floats, ws_bytes = plan.bucketed_sizes([b[1] for b in buckets])
+    work = torch.empty((N, work_floats), dtype=torch.float32, device=dev)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.full((N, d), float("nan"), dtype=torch.float32, device=dev)
+    C.ring_simulate_bucketed(plan, buckets, to_device(g), work, ws, out)
+    sync()
+    gpu = out.double().cpu().numpy()
+    for off, ln in buckets:
+        ref = OR.allreduce(g[:, off:off + ln], U, R)
+        assert max_rel_l2(gpu[:, off:off + ln], ref) < 1e-4
+
+
+def test_copy_kernel():
+    torch, dev = torch_dev()
+    for n in (1, 7, 4096, 1_000_003):
+        src = torch.randn(n + 1, device=dev)[1:] if n % 2 else torch.randn(n, device=dev)
+        dst = torch.empty_like(src)
+        C.copy_f32(dst, src)
+        sync()
+        assert bool((dst == src).all())
