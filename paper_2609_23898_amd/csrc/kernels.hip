@@ -101,6 +101,68 @@ __device__ inline void store_tile(float *__restrict__ row, size_t row_off, size_
     }
 }
 
+// ---- MFMA operand helpers ------------------------------------------------------
+// A fragments (coefficients) are either held in registers for up to four
+// M-tiles, or staged in LDS so that one ds_read_b128 fetches four K-steps.
+// Interior 64-position blocks (the uniform common case) use unmasked
+// non-temporal 16-byte loads and stores; tail blocks take the masked path.
+
+constexpr int kMaxRegTiles = 4;
+
+__device__ inline v4f nt_load(const float *ptr) { return __builtin_nontemporal_load(reinterpret_cast<const v4f *>(ptr)); }
+__device__ inline void nt_store(float *ptr, v4f v) { __builtin_nontemporal_store(v, reinterpret_cast<v4f *>(ptr)); }
+
+// Wave-uniform base pointer plus a 32-bit per-lane byte offset: the form of a
+// global access with a scalar base register, which keeps one VGPR of address
+// per lane instead of a 64-bit pointer per row.  opaque() hides the offset's
+// loop invariance (it emits no instruction), so the compiler cannot hoist
+// base + offset into one live 64-bit pointer per row across the block loop.
+__device__ inline uint32_t opaque(uint32_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+__device__ inline v4f nt_load_off(const float *ubase, uint32_t lane_bytes) {
+    return __builtin_nontemporal_load(reinterpret_cast<const v4f *>(reinterpret_cast<const char *>(ubase) + lane_bytes));
+}
+__device__ inline void nt_store_off(float *ubase, uint32_t lane_bytes, v4f v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<v4f *>(reinterpret_cast<char *>(ubase) + lane_bytes));
+}
+
+// Copies nmt M-tiles of fragments [mt][ks][lane] into LDS as [mt][ks/4][lane][ks%4].
+__device__ inline void stage_fragments(float *sfrag, const float *gfrag, int nmt, int KSx) {
+    const int KS4 = (KSx + 3) / 4;
+    const int total = nmt * KS4 * 64 * 4;
+    for (int idx = threadIdx.x; idx < total; idx += kThreads) {
+        const int r = idx & 3, ln = (idx >> 2) & 63, q = (idx >> 8) % KS4, mt = (idx >> 8) / KS4;
+        const int ks = q * 4 + r;
+        sfrag[idx] = ks < KSx ? gfrag[((size_t)mt * KSx + ks) * 64 + ln] : 0.f;
+    }
+}
+
+// One M-tile: 4 MFMA chains (one per position component t) over the K-steps.
+template <int KS, bool AREG>
+__device__ inline void mtile_mma(v4f (&acc)[4], const v4f (&b)[KS], const float (&av)[KS], const float *sfr,
+                                 int KSx, int lane) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < (KS + 3) / 4; ++q) {
+        v4f aq = {0.f, 0.f, 0.f, 0.f};
+        if (!AREG && q * 4 < KSx) aq = *reinterpret_cast<const v4f *>(sfr + ((size_t)q * 64 + lane) * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int ks = q * 4 + r;
+            if (ks < KS && ks < KSx) {
+                const float a = AREG ? av[ks] : aq[r];
+                acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b[ks][0], acc[0], 0, 0, 0);
+                acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b[ks][1], acc[1], 0, 0, 0);
+                acc[2] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b[ks][2], acc[2], 0, 0, 0);
+                acc[3] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b[ks][3], acc[3], 0, 0, 0);
+            }
+        }
+    }
+}
+
 // ---- K1: encode -----------------------------------------------------------------
 
 struct EncParams {
@@ -112,56 +174,73 @@ struct EncParams {
     int N, c, MT, KSe;
     int mt0, mt1;           // M-tiles handled by this launch
     int wg_per_worker;
-    size_t nblk;            // 64-position blocks per row
+    size_t blk0, blk1;      // 64-position blocks [blk0, blk1) of every row
 };
 
-template <int KS, bool VEC>
+// FAST: interior blocks only (full rows, no masks, non-temporal 16-byte
+// accesses); otherwise the masked path for tails and the scalar layout.
+template <int KS, bool VEC, bool AREG, bool FAST>
 __global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
     extern __shared__ float sfrag[];
     const int worker = blockIdx.x / a.wg_per_worker;
     const int wg = blockIdx.x - worker * a.wg_per_worker;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int nmt = a.mt1 - a.mt0;
-    const float *gfrag = a.frag + ((size_t)worker * a.MT + a.mt0) * a.KSe * 64;
-    for (int t = threadIdx.x; t < nmt * a.KSe * 64; t += kThreads) sfrag[t] = gfrag[t];
-    __syncthreads();
+    const int KSx = a.KSe, KS4 = (KSx + 3) / 4;
+    const float *gfrag = a.frag + ((size_t)worker * a.MT + a.mt0) * KSx * 64;
+    float av[AREG ? kMaxRegTiles : 1][KS];
+    if (AREG) {
+#pragma unroll
+        for (int mt = 0; mt < kMaxRegTiles; ++mt)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                av[mt][ks] = (mt < nmt && ks < KSx) ? gfrag[((size_t)mt * KSx + ks) * 64 + lane] : 0.f;
+    } else {
+        stage_fragments(sfrag, gfrag, nmt, KSx);
+        __syncthreads();
+    }
     const float *src = a.grads + (size_t)worker * a.ld_g;
     float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
     float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;   // worker's first pool slot
     const size_t p = a.sb.p;
-    for (size_t blk = (size_t)wg * kWaves + wave; blk < a.nblk; blk += (size_t)a.wg_per_worker * kWaves) {
+    for (size_t blk = a.blk0 + (size_t)wg * kWaves + wave; blk < a.blk1; blk += (size_t)a.wg_per_worker * kWaves) {
         const size_t e0 = blk * 64;
         v4f b[KS];
+        if (FAST) {
+            // K-steps past c/4 re-read the last real one; their coefficients are zero
+            const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int l = ks * 4 + krow;
-            if (ks < a.KSe && l < a.c)
-                b[ks] = load_tile<VEC>(src + (size_t)l * p, (size_t)l * p, e0, col, p, a.d);
-            else
-                b[ks] = v4f{0.f, 0.f, 0.f, 0.f};
-        }
-        for (int mt = 0; mt < nmt; ++mt) {
-            v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0, acc2 = acc0, acc3 = acc0;
-            const float *fr = sfrag + (size_t)mt * a.KSe * 64 + lane;
+            for (int ks = 0; ks < KS; ++ks)
+                b[ks] = nt_load_off(src + e0 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+        } else {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                if (ks < a.KSe) {
-                    const float av = fr[ks * 64];
-                    acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][0], acc0, 0, 0, 0);
-                    acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][1], acc1, 0, 0, 0);
-                    acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][2], acc2, 0, 0, 0);
-                    acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][3], acc3, 0, 0, 0);
-                }
+                const int l = ks * 4 + krow;
+                b[ks] = (ks < KSx && l < a.c) ? load_tile<VEC>(src + (size_t)l * p, (size_t)l * p, e0, col, p, a.d)
+                                              : v4f{0.f, 0.f, 0.f, 0.f};
             }
-            // D fragment: lane (krow, col), register r holds output row 4 krow + r.
+        }
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int j = (a.mt0 + mt) * 16 + krow * 4 + r;
-                if (j < a.c) {
-                    const v4f v = {acc0[r], acc1[r], acc2[r], acc3[r]};
-                    store_tile<VEC>(dst + (size_t)j * p, 0, e0, col, p, p, v);
-                    if (j == 0) store_tile<VEC>(x1, 0, e0, col, p, p, v);
+        for (int mt = 0; mt < (AREG ? kMaxRegTiles : 1); ++mt) {
+            for (int m2 = mt; m2 < (AREG ? mt + 1 : nmt); ++m2) {
+                if (m2 >= nmt) break;
+                v4f acc[4];
+                mtile_mma<KS, AREG>(acc, b, av[AREG ? mt : 0], sfrag + (size_t)m2 * KS4 * 256, KSx, lane);
+                // D fragment: lane (krow, col), register r holds output row 4 krow + r.
+                const int jt = (a.mt0 + m2) * 16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int j = jt + krow * 4 + r;
+                    const v4f v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+                    if (FAST) {
+                        nt_store_off(dst + e0 + (size_t)(jt + r) * p, lane_out, v);   // j < c: 16 | c
+                        if (j == 0) nt_store_off(x1 + e0, (uint32_t)(4 * col * sizeof(float)), v);
+                    } else if (j < a.c) {
+                        store_tile<VEC>(dst + (size_t)j * p, 0, e0, col, p, p, v);
+                        if (j == 0) store_tile<VEC>(x1, 0, e0, col, p, p, v);
+                    }
                 }
             }
         }
@@ -172,6 +251,8 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
 // MODE 0: x_next = recv + add            (rounds 1..N-1)
 // MODE 1: x_next = (recv - sub) + add    (rounds N..c-1)
 // MODE 2: x_next = recv - sub            (rounds c..L-1)
+// One 16-byte element per thread, non-temporal loads and stores, and a
+// one-shot grid: the fastest streaming shape measured on MI355X.
 
 struct RoundParams {
     SlotBase sb;
@@ -179,59 +260,32 @@ struct RoundParams {
     int wg_per_worker;
 };
 
-constexpr int kRoundUnroll = 4;
+constexpr int kRoundThreads = 128;
 
 template <int MODE, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_round(RoundParams a) {
+__global__ __launch_bounds__(kRoundThreads) void k_round(RoundParams a) {
     const int worker = blockIdx.x / a.wg_per_worker;
     const int wg = blockIdx.x - worker * a.wg_per_worker;
     const RoundOp op = a.ops[worker];
-    const float *__restrict__ recv = a.sb.ptr(op.recv);
+    const float *recv = a.sb.ptr(op.recv);
     const float *sub = MODE >= 1 ? a.sb.ptr(op.sub) : nullptr;   // aliases dst (in place)
-    const float *__restrict__ add = MODE <= 1 ? a.sb.ptr(op.add) : nullptr;
+    const float *add = MODE <= 1 ? a.sb.ptr(op.add) : nullptr;
     float *dst = a.sb.ptr(op.dst);
     const size_t p = a.sb.p;
-    const size_t stride = (size_t)a.wg_per_worker * kThreads * kRoundUnroll;
     if (VEC) {
-        const size_t n4 = p / 4;
-        const v4f *r4 = reinterpret_cast<const v4f *>(recv);
-        const v4f *s4 = reinterpret_cast<const v4f *>(sub);
-        const v4f *a4 = reinterpret_cast<const v4f *>(add);
-        v4f *d4 = reinterpret_cast<v4f *>(dst);
-        for (size_t base = (size_t)wg * kThreads * kRoundUnroll + threadIdx.x; base < n4; base += stride) {
-            v4f x[kRoundUnroll], y[kRoundUnroll], z[kRoundUnroll];
-#pragma unroll
-            for (int u = 0; u < kRoundUnroll; ++u) {
-                const size_t i = base + (size_t)u * kThreads;
-                if (i < n4) {
-                    x[u] = r4[i];
-                    if (MODE >= 1) y[u] = s4[i];
-                    if (MODE <= 1) z[u] = a4[i];
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kRoundUnroll; ++u) {
-                const size_t i = base + (size_t)u * kThreads;
-                if (i < n4) {
-                    v4f v = x[u];
-                    if (MODE >= 1) v = v - y[u];
-                    if (MODE <= 1) v = v + z[u];
-                    d4[i] = v;
-                }
-            }
+        const size_t i = ((size_t)wg * kRoundThreads + threadIdx.x) * 4;
+        if (i < p) {
+            v4f v = nt_load(recv + i);
+            if (MODE >= 1) v = v - nt_load(sub + i);
+            if (MODE <= 1) v = v + nt_load(add + i);
+            nt_store(dst + i, v);
         }
     } else {
-        for (size_t base = (size_t)wg * kThreads * kRoundUnroll + threadIdx.x; base < p; base += stride) {
-#pragma unroll
-            for (int u = 0; u < kRoundUnroll; ++u) {
-                const size_t i = base + (size_t)u * kThreads;
-                if (i < p) {
-                    float v = recv[i];
-                    if (MODE >= 1) v = v - sub[i];
-                    if (MODE <= 1) v = v + add[i];
-                    dst[i] = v;
-                }
-            }
+        for (size_t i = (size_t)wg * kRoundThreads + threadIdx.x; i < p; i += (size_t)a.wg_per_worker * kRoundThreads) {
+            float v = recv[i];
+            if (MODE >= 1) v = v - sub[i];
+            if (MODE <= 1) v = v + add[i];
+            dst[i] = v;
         }
     }
 }
@@ -248,56 +302,70 @@ struct DecParams {
     int N, c, K, MT, KSd;
     int mt0, mt1;
     int wg_per_worker;
-    size_t nblk;
+    size_t blk0, blk1;
 };
 
-template <int KS, bool VEC>
+template <int KS, bool VEC, bool AREG, bool FAST>
 __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
     extern __shared__ float smem[];
     const int worker = blockIdx.x / a.wg_per_worker;
     const int wg = blockIdx.x - worker * a.wg_per_worker;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int nmt = a.mt1 - a.mt0;
-    const size_t nfrag = (size_t)nmt * a.KSd * 64;
+    const int KSx = a.KSd, KS4 = (KSx + 3) / 4;
+    const size_t nfrag = AREG ? 0 : (size_t)nmt * KS4 * 256;
     float *sfrag = smem;
     const float **srow = reinterpret_cast<const float **>(smem + ((nfrag + 1) & ~(size_t)1));
-    const float *gfrag = a.frag + ((size_t)worker * a.MT + a.mt0) * a.KSd * 64;
-    for (size_t t = threadIdx.x; t < nfrag; t += kThreads) sfrag[t] = gfrag[t];
-    for (int t = threadIdx.x; t < a.K; t += kThreads) srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + t]);
+    const float *gfrag = a.frag + ((size_t)worker * a.MT + a.mt0) * KSx * 64;
+    float av[AREG ? kMaxRegTiles : 1][KS];
+    if (AREG) {
+#pragma unroll
+        for (int mt = 0; mt < kMaxRegTiles; ++mt)
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+                av[mt][ks] = (mt < nmt && ks < KSx) ? gfrag[((size_t)mt * KSx + ks) * 64 + lane] : 0.f;
+    } else {
+        stage_fragments(sfrag, gfrag, nmt, KSx);
+    }
+    // rows K..4 KSx-1 of the last K-step repeat row K-1; their coefficients are zero
+    for (int t = threadIdx.x; t < 4 * KSx; t += kThreads)
+        srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
     __syncthreads();
     float *out = a.out + (size_t)worker * a.ld_o;
     const size_t p = a.sb.p;
-    for (size_t blk = (size_t)wg * kWaves + wave; blk < a.nblk; blk += (size_t)a.wg_per_worker * kWaves) {
+    for (size_t blk = a.blk0 + (size_t)wg * kWaves + wave; blk < a.blk1; blk += (size_t)a.wg_per_worker * kWaves) {
         const size_t e0 = blk * 64;
         v4f b[KS];
+        if (FAST) {
+            const size_t off = e0 + 4 * (size_t)col;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const int k = ks * 4 + krow;
-            if (ks < a.KSd && k < a.K)
-                b[ks] = load_tile<VEC>(srow[k], 0, e0, col, p, p);
-            else
-                b[ks] = v4f{0.f, 0.f, 0.f, 0.f};
-        }
-        for (int mt = 0; mt < nmt; ++mt) {
-            v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0, acc2 = acc0, acc3 = acc0;
-            const float *fr = sfrag + (size_t)mt * a.KSd * 64 + lane;
+            for (int ks = 0; ks < KS; ++ks)
+                b[ks] = ks < KSx ? nt_load(srow[ks * 4 + krow] + off) : v4f{0.f, 0.f, 0.f, 0.f};
+        } else {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                if (ks < a.KSd) {
-                    const float av = fr[ks * 64];
-                    acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][0], acc0, 0, 0, 0);
-                    acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][1], acc1, 0, 0, 0);
-                    acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][2], acc2, 0, 0, 0);
-                    acc3 = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][3], acc3, 0, 0, 0);
-                }
+                const int k = ks * 4 + krow;
+                b[ks] = (ks < KSx && k < a.K) ? load_tile<VEC>(srow[k], 0, e0, col, p, p) : v4f{0.f, 0.f, 0.f, 0.f};
             }
+        }
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int m = (a.mt0 + mt) * 16 + krow * 4 + r;
-                if (m < a.c) {
-                    const v4f v = {acc0[r], acc1[r], acc2[r], acc3[r]};
-                    store_tile<VEC>(out + (size_t)m * p, (size_t)m * p, e0, col, p, a.d, v);
+        for (int mt = 0; mt < (AREG ? kMaxRegTiles : 1); ++mt) {
+            for (int m2 = mt; m2 < (AREG ? mt + 1 : nmt); ++m2) {
+                if (m2 >= nmt) break;
+                v4f acc[4];
+                mtile_mma<KS, AREG>(acc, b, av[AREG ? mt : 0], sfrag + (size_t)m2 * KS4 * 256, KSx, lane);
+                const int mtile = (a.mt0 + m2) * 16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int m = mtile + krow * 4 + r;
+                    const v4f v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+                    if (FAST) {
+                        nt_store_off(out + e0 + (size_t)(mtile + r) * p, lane_out, v);   // m < c: 16 | c
+                    } else if (m < a.c) {
+                        store_tile<VEC>(out + (size_t)m * p, (size_t)m * p, e0, col, p, a.d, v);
+                    }
                 }
             }
         }
@@ -361,21 +429,11 @@ __global__ __launch_bounds__(kThreads) void k_norms(int N, size_t d, const float
 
 // ---- copy ----------------------------------------------------------------------
 
-__global__ __launch_bounds__(kThreads) void k_copy4(v4f *__restrict__ dst, const v4f *__restrict__ src, size_t n4) {
-    const size_t stride = (size_t)gridDim.x * kThreads * kRoundUnroll;
-    for (size_t base = (size_t)blockIdx.x * kThreads * kRoundUnroll + threadIdx.x; base < n4; base += stride) {
-        v4f x[kRoundUnroll];
-#pragma unroll
-        for (int u = 0; u < kRoundUnroll; ++u) {
-            const size_t i = base + (size_t)u * kThreads;
-            if (i < n4) x[u] = src[i];
-        }
-#pragma unroll
-        for (int u = 0; u < kRoundUnroll; ++u) {
-            const size_t i = base + (size_t)u * kThreads;
-            if (i < n4) dst[i] = x[u];
-        }
-    }
+constexpr int kCopyThreads = 64;
+
+__global__ __launch_bounds__(kCopyThreads) void k_copy4(float *__restrict__ dst, const float *__restrict__ src, size_t n4) {
+    const size_t i = (size_t)blockIdx.x * kCopyThreads + threadIdx.x;
+    if (i < n4) nt_store(dst + 4 * i, nt_load(src + 4 * i));
 }
 
 __global__ void k_copy1(float *__restrict__ dst, const float *__restrict__ src, size_t n) {
@@ -469,23 +527,82 @@ int wg_for(size_t nblk) {
     return (int)w;
 }
 
-template <int KS>
-void launch_encode_ks(const EncParams &a, bool vec, size_t lds, hipStream_t s, dim3 grid) {
-    if (vec) hipLaunchKernelGGL((k_encode<KS, true>), grid, dim3(kThreads), lds, s, a);
-    else hipLaunchKernelGGL((k_encode<KS, false>), grid, dim3(kThreads), lds, s, a);
+// Launch flavours: interior blocks (FAST), masked 16-byte layout, scalar layout.
+enum class Path { kFast, kMaskedVec, kScalar };
+
+template <int KS, bool AREG>
+void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+    if (path == Path::kFast) hipLaunchKernelGGL((k_encode<KS, true, AREG, true>), grid, dim3(kThreads), lds, s, a);
+    else if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_encode<KS, true, AREG, false>), grid, dim3(kThreads), lds, s, a);
+    else hipLaunchKernelGGL((k_encode<KS, false, AREG, false>), grid, dim3(kThreads), lds, s, a);
 }
 
 template <int KS>
-void launch_decode_ks(const DecParams &a, bool vec, size_t lds, hipStream_t s, dim3 grid) {
-    if (vec) hipLaunchKernelGGL((k_decode<KS, true>), grid, dim3(kThreads), lds, s, a);
-    else hipLaunchKernelGGL((k_decode<KS, false>), grid, dim3(kThreads), lds, s, a);
+void launch_decode_ks(const DecParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+    if (path == Path::kFast) hipLaunchKernelGGL((k_decode<KS, true, false, true>), grid, dim3(kThreads), lds, s, a);
+    else if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_decode<KS, true, false, false>), grid, dim3(kThreads), lds, s, a);
+    else hipLaunchKernelGGL((k_decode<KS, false, false, false>), grid, dim3(kThreads), lds, s, a);
 }
 
-// M-tiles per launch so that their fragments fit the LDS budget.
+// M-tiles per launch so that their staged fragments fit the LDS budget.
 int mtiles_per_launch(int MT, int KS, size_t extra) {
-    size_t per = (size_t)KS * 64 * sizeof(float);
-    int n = (int)((kLdsBudget - extra) / per);
+    const size_t per = (size_t)((KS + 3) / 4) * 256 * sizeof(float);
+    const int n = (int)((kLdsBudget - extra) / per);
     return std::max(1, std::min(MT, n));
+}
+
+// Blocks [0, interior) need no masks: the whole 64-position block lies inside
+// the chunk (e0 + 64 <= p) and inside the gradient for every chunk
+// ((c-1) p + e0 + 64 <= d), and c is a multiple of 16 so every row of every
+// M-tile is a real chunk; beyond them only the tail of the last block and the
+// zero pad of the last chunk remain (at most a few blocks).
+struct BlockSplit {
+    size_t interior, total;
+    Path tail;
+};
+
+BlockSplit split_blocks(const cerar_plan *plan, size_t p, size_t d, bool vec) {
+    BlockSplit b;
+    b.total = (p + 63) / 64;
+    b.interior = 0;
+    b.tail = vec ? Path::kMaskedVec : Path::kScalar;
+    const size_t last_row = (size_t)(plan->c - 1) * p;
+    // lane offsets of the fast path (up to 12 p + 64 floats) must fit 31 bits
+    const bool small_rows = (12 * p + 64) * sizeof(float) < ((size_t)1 << 31);
+    // the unmasked stores write all 16 rows of every M-tile: c must fill whole tiles
+    if (vec && small_rows && plan->c % 16 == 0 && d > last_row) b.interior = std::min(p, d - last_row) / 64;
+    return b;
+}
+
+template <class Params, class Launch>
+int launch_split(Params a, const BlockSplit &bs, size_t lds, hipStream_t s, int N, Launch launch) {
+    if (bs.interior > 0) {
+        a.blk0 = 0;
+        a.blk1 = bs.interior;
+        a.wg_per_worker = wg_for(bs.interior);
+        launch(a, Path::kFast, lds, s, dim3((unsigned)(N * a.wg_per_worker)));
+    }
+    if (bs.total > bs.interior) {
+        a.blk0 = bs.interior;
+        a.blk1 = bs.total;
+        a.wg_per_worker = wg_for(bs.total - bs.interior);
+        launch(a, bs.tail, lds, s, dim3((unsigned)(N * a.wg_per_worker)));
+    }
+    return CERAR_OK;
+}
+
+template <int KS, bool AREG>
+int encode_ks(const EncParams &a, const BlockSplit &bs, size_t lds, hipStream_t s, int N) {
+    return launch_split(a, bs, lds, s, N, [](const EncParams &x, Path path, size_t l, hipStream_t st, dim3 g) {
+        launch_encode_ks<KS, AREG>(x, path, l, st, g);
+    });
+}
+
+template <int KS>
+int decode_ks(const DecParams &a, const BlockSplit &bs, size_t lds, hipStream_t s, int N) {
+    return launch_split(a, bs, lds, s, N, [](const DecParams &x, Path path, size_t l, hipStream_t st, dim3 g) {
+        launch_decode_ks<KS>(x, path, l, st, g);
+    });
 }
 
 int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, size_t d,
@@ -500,25 +617,27 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     a.c = plan->c;
     a.MT = plan->MT;
     a.KSe = plan->KSe;
-    a.nblk = (g.p + 63) / 64;
-    a.wg_per_worker = wg_for(a.nblk);
     const bool vec = g.vec && (ld_grads % 4 == 0) && aligned16(grads);
-    const dim3 grid((unsigned)(plan->N * a.wg_per_worker));
-    const int step = mtiles_per_launch(plan->MT, plan->KSe, 0);
-    for (int mt0 = 0; mt0 < plan->MT; mt0 += step) {
-        a.mt0 = mt0;
-        a.mt1 = std::min(plan->MT, mt0 + step);
-        const size_t lds = (size_t)(a.mt1 - a.mt0) * plan->KSe * 64 * sizeof(float);
-        const int ks = plan->KSe;
-        if (ks <= 1) launch_encode_ks<1>(a, vec, lds, s, grid);
-        else if (ks <= 2) launch_encode_ks<2>(a, vec, lds, s, grid);
-        else if (ks <= 4) launch_encode_ks<4>(a, vec, lds, s, grid);
-        else if (ks <= 8) launch_encode_ks<8>(a, vec, lds, s, grid);
-        else if (ks <= 16) launch_encode_ks<16>(a, vec, lds, s, grid);
-        else if (ks <= 24) launch_encode_ks<24>(a, vec, lds, s, grid);
-        else launch_encode_ks<32>(a, vec, lds, s, grid);
-        HIP_TRY(hipGetLastError(), "launch encode");
+    const BlockSplit bs = split_blocks(plan, g.p, d, vec);
+    const int N = plan->N, ks = plan->KSe;
+    a.mt0 = 0;
+    a.mt1 = plan->MT;
+    if (plan->MT <= kMaxRegTiles) {                  // c <= 64: coefficients in registers
+        if (ks <= 1) encode_ks<1, true>(a, bs, 0, s, N);
+        else if (ks <= 2) encode_ks<2, true>(a, bs, 0, s, N);
+        else if (ks <= 4) encode_ks<4, true>(a, bs, 0, s, N);
+        else if (ks <= 8) encode_ks<8, true>(a, bs, 0, s, N);
+        else encode_ks<16, true>(a, bs, 0, s, N);
+    } else {
+        // All M-tiles in one launch (c <= 128 fits the LDS budget), which an
+        // in-place encode needs: every input row is read before any is written.
+        if (mtiles_per_launch(plan->MT, ks, 0) < plan->MT)
+            return fail(CERAR_E_INVAL, "c=%d exceeds the encode's LDS budget", plan->c);
+        const size_t lds = (size_t)plan->MT * ((ks + 3) / 4) * 256 * sizeof(float);
+        if (ks <= 24) encode_ks<24, false>(a, bs, lds, s, N);
+        else encode_ks<32, false>(a, bs, lds, s, N);
     }
+    HIP_TRY(hipGetLastError(), "launch encode");
     return CERAR_OK;
 }
 
@@ -529,19 +648,22 @@ int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &
     RoundParams a;
     a.sb = slot_base(plan, g, work, ld_work, ws);
     a.ops = dc->rounds + (size_t)k * N;
-    const size_t units = g.vec ? g.p / 4 : g.p;
-    size_t w = (units + (size_t)kThreads * kRoundUnroll - 1) / ((size_t)kThreads * kRoundUnroll);
-    a.wg_per_worker = (int)std::max<size_t>(1, std::min<size_t>(w, 1 << 20));
+    if (g.vec) {
+        a.wg_per_worker = (int)((g.p / 4 + kRoundThreads - 1) / kRoundThreads);
+    } else {
+        a.wg_per_worker = (int)std::min<size_t>((g.p + kRoundThreads - 1) / kRoundThreads, 1 << 16);
+    }
+    a.wg_per_worker = std::max(1, a.wg_per_worker);
     const dim3 grid((unsigned)(N * a.wg_per_worker));
     const int mode = (k <= N - 1) ? 0 : (k + 1 <= c ? 1 : 2);
     if (g.vec) {
-        if (mode == 0) hipLaunchKernelGGL((k_round<0, true>), grid, dim3(kThreads), 0, s, a);
-        else if (mode == 1) hipLaunchKernelGGL((k_round<1, true>), grid, dim3(kThreads), 0, s, a);
-        else hipLaunchKernelGGL((k_round<2, true>), grid, dim3(kThreads), 0, s, a);
+        if (mode == 0) hipLaunchKernelGGL((k_round<0, true>), grid, dim3(kRoundThreads), 0, s, a);
+        else if (mode == 1) hipLaunchKernelGGL((k_round<1, true>), grid, dim3(kRoundThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_round<2, true>), grid, dim3(kRoundThreads), 0, s, a);
     } else {
-        if (mode == 0) hipLaunchKernelGGL((k_round<0, false>), grid, dim3(kThreads), 0, s, a);
-        else if (mode == 1) hipLaunchKernelGGL((k_round<1, false>), grid, dim3(kThreads), 0, s, a);
-        else hipLaunchKernelGGL((k_round<2, false>), grid, dim3(kThreads), 0, s, a);
+        if (mode == 0) hipLaunchKernelGGL((k_round<0, false>), grid, dim3(kRoundThreads), 0, s, a);
+        else if (mode == 1) hipLaunchKernelGGL((k_round<1, false>), grid, dim3(kRoundThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_round<2, false>), grid, dim3(kRoundThreads), 0, s, a);
     }
     HIP_TRY(hipGetLastError(), "launch round");
     return CERAR_OK;
@@ -561,26 +683,24 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     a.K = plan->L + 1;
     a.MT = plan->MT;
     a.KSd = plan->KSd;
-    a.nblk = (g.p + 63) / 64;
-    a.wg_per_worker = wg_for(a.nblk);
     const bool vec = g.vec && (ld_out % 4 == 0) && aligned16(out);
-    const dim3 grid((unsigned)(plan->N * a.wg_per_worker));
-    const size_t rows_bytes = (size_t)a.K * sizeof(float *) + 16;
-    const int step = mtiles_per_launch(plan->MT, plan->KSd, rows_bytes);
+    const BlockSplit bs = split_blocks(plan, g.p, d, vec);
+    const int N = plan->N, ks = plan->KSd;
+    const size_t rows_bytes = (size_t)4 * ks * sizeof(float *) + 16;
+    const int step = mtiles_per_launch(plan->MT, ks, rows_bytes);
     for (int mt0 = 0; mt0 < plan->MT; mt0 += step) {
         a.mt0 = mt0;
         a.mt1 = std::min(plan->MT, mt0 + step);
-        const size_t lds = (size_t)(a.mt1 - a.mt0) * plan->KSd * 64 * sizeof(float) + rows_bytes;
-        const int ks = plan->KSd;
-        if (ks <= 4) launch_decode_ks<4>(a, vec, lds, s, grid);
-        else if (ks <= 8) launch_decode_ks<8>(a, vec, lds, s, grid);
-        else if (ks <= 12) launch_decode_ks<12>(a, vec, lds, s, grid);
-        else if (ks <= 16) launch_decode_ks<16>(a, vec, lds, s, grid);
-        else if (ks <= 20) launch_decode_ks<20>(a, vec, lds, s, grid);
-        else if (ks <= 24) launch_decode_ks<24>(a, vec, lds, s, grid);
-        else if (ks <= 32) launch_decode_ks<32>(a, vec, lds, s, grid);
-        else if (ks <= 40) launch_decode_ks<40>(a, vec, lds, s, grid);
-        else launch_decode_ks<48>(a, vec, lds, s, grid);
+        const size_t lds = (size_t)(a.mt1 - a.mt0) * ((ks + 3) / 4) * 256 * sizeof(float) + rows_bytes;
+        if (ks <= 4) decode_ks<4>(a, bs, lds, s, N);
+        else if (ks <= 8) decode_ks<8>(a, bs, lds, s, N);
+        else if (ks <= 12) decode_ks<12>(a, bs, lds, s, N);
+        else if (ks <= 16) decode_ks<16>(a, bs, lds, s, N);
+        else if (ks <= 20) decode_ks<20>(a, bs, lds, s, N);
+        else if (ks <= 24) decode_ks<24>(a, bs, lds, s, N);
+        else if (ks <= 32) decode_ks<32>(a, bs, lds, s, N);
+        else if (ks <= 40) decode_ks<40>(a, bs, lds, s, N);
+        else decode_ks<48>(a, bs, lds, s, N);
         HIP_TRY(hipGetLastError(), "launch decode");
     }
     return CERAR_OK;
@@ -734,9 +854,9 @@ extern "C" int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stre
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (n % 4 == 0 && aligned16(dst) && aligned16(src)) {
         const size_t n4 = n / 4;
-        size_t blocks = (n4 + (size_t)kThreads * kRoundUnroll - 1) / ((size_t)kThreads * kRoundUnroll);
-        blocks = std::max<size_t>(1, std::min<size_t>(blocks, 1 << 20));
-        hipLaunchKernelGGL(k_copy4, dim3((unsigned)blocks), dim3(kThreads), 0, s, (v4f *)dst, (const v4f *)src, n4);
+        const size_t blocks = (n4 + kCopyThreads - 1) / kCopyThreads;
+        if (blocks > 0x7fffffffu) return fail(CERAR_E_INVAL, "copy of %zu floats is too large for one launch", n);
+        hipLaunchKernelGGL(k_copy4, dim3((unsigned)blocks), dim3(kCopyThreads), 0, s, dst, src, n4);
     } else {
         size_t blocks = std::max<size_t>(1, std::min<size_t>((n + kThreads - 1) / kThreads, 1 << 16));
         hipLaunchKernelGGL(k_copy1, dim3((unsigned)blocks), dim3(kThreads), 0, s, dst, src, n);
