@@ -108,6 +108,7 @@ __device__ inline void store_tile(float *__restrict__ row, size_t row_off, size_
 // non-temporal 16-byte loads and stores; tail blocks take the masked path.
 
 constexpr int kMaxRegTiles = 4;
+constexpr int kMaxDecodeKS = 48;   // K = c + N - 1 <= 191 observations
 
 __device__ inline v4f nt_load(const float *ptr) { return __builtin_nontemporal_load(reinterpret_cast<const v4f *>(ptr)); }
 __device__ inline void nt_store(float *ptr, v4f v) { __builtin_nontemporal_store(v, reinterpret_cast<v4f *>(ptr)); }
@@ -163,6 +164,41 @@ __device__ inline void mtile_mma(v4f (&acc)[4], const v4f (&b)[KS], const float 
     }
 }
 
+// Guard-free variant for the pipelined kernels: all KS K-steps run, the
+// fragments in LDS are zero beyond the plan's K-steps (staged with KSpad = KS),
+// so the reduction needs no runtime test and the wait counters stay exact.
+template <int KS>
+__device__ inline void mtile_mma_lds(v4f (&acc)[4], const v4f (&b)[KS], const float *sfr, int lane) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < (KS + 3) / 4; ++q) {
+        const v4f aq = *reinterpret_cast<const v4f *>(sfr + ((size_t)q * 64 + lane) * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int ks = q * 4 + r;
+            if (ks < KS) {
+                acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][0], acc[0], 0, 0, 0);
+                acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][1], acc[1], 0, 0, 0);
+                acc[2] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][2], acc[2], 0, 0, 0);
+                acc[3] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][3], acc[3], 0, 0, 0);
+            }
+        }
+    }
+}
+
+// Copies nmt M-tiles of fragments [mt][ks][lane] (KSx K-steps) into LDS as
+// [mt][q][lane][r], ks = 4q + r, zero-padded to KSpad K-steps.
+__device__ inline void stage_fragments_padded(float *sfrag, const float *gfrag, int nmt, int KSx, int KSpad) {
+    const int Q = (KSpad + 3) / 4;
+    const int total = nmt * Q * 256;
+    for (int idx = threadIdx.x; idx < total; idx += kThreads) {
+        const int r = idx & 3, ln = (idx >> 2) & 63, q = (idx >> 8) % Q, mt = (idx >> 8) / Q;
+        const int ks = q * 4 + r;
+        sfrag[idx] = ks < KSx ? gfrag[((size_t)mt * KSx + ks) * 64 + ln] : 0.f;
+    }
+}
+
 // ---- K1: encode -----------------------------------------------------------------
 
 struct EncParams {
@@ -182,8 +218,8 @@ struct EncParams {
 template <int KS, bool VEC, bool AREG, bool FAST>
 __global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
     extern __shared__ float sfrag[];
-    const int worker = blockIdx.x / a.wg_per_worker;
-    const int wg = blockIdx.x - worker * a.wg_per_worker;
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int nmt = a.mt1 - a.mt0;
@@ -247,6 +283,65 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
     }
 }
 
+// Pipelined interior encode for c <= 64 (up to 4 M-tiles): the coefficients
+// stay in LDS, all M-tile accumulators stay in AGPRs, and the next block's
+// loads are issued before the current block's stores, so every wave keeps
+// loads in flight while its stores drain.
+template <int KS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 16 ? 3 : 2))) void k_encode_pipe(EncParams a) {
+    extern __shared__ float sfrag[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int MT = a.mt1 - a.mt0;                       // <= kMaxRegTiles
+    const int KSx = a.KSe;
+    constexpr int Q = (KS + 3) / 4;
+    stage_fragments_padded(sfrag, a.frag + ((size_t)worker * a.MT + a.mt0) * KSx * 64, MT, KSx, KS);
+    __syncthreads();
+    const float *src = a.grads + (size_t)worker * a.ld_g;
+    float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
+    float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
+    const size_t p = a.sb.p;
+    const size_t stride = (size_t)a.wg_per_worker * kWaves;
+    size_t blk = a.blk0 + (size_t)wg * kWaves + wave;
+    if (blk >= a.blk1) return;
+    v4f b[KS];
+    {
+        const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_off(src + blk * 64 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+    }
+    while (true) {
+        const size_t e0 = blk * 64;
+        v4f acc[kMaxRegTiles][4];
+#pragma unroll
+        for (int mt = 0; mt < kMaxRegTiles; ++mt)
+            if (mt < MT) mtile_mma_lds<KS>(acc[mt], b, sfrag + (size_t)mt * Q * 256, lane);
+        const size_t next = blk + stride;
+        if (next < a.blk1) {
+            const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_off(src + next * 64 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+        }
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+        for (int mt = 0; mt < kMaxRegTiles; ++mt) {
+            if (mt < MT) {
+                const int jt = (a.mt0 + mt) * 16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const v4f v = {acc[mt][0][r], acc[mt][1][r], acc[mt][2][r], acc[mt][3][r]};
+                    nt_store_off(dst + e0 + (size_t)(jt + r) * p, lane_out, v);   // 16 | c
+                    if (jt + krow * 4 + r == 0) nt_store_off(x1 + e0, (uint32_t)(4 * col * sizeof(float)), v);
+                }
+            }
+        }
+        if (next >= a.blk1) break;
+        blk = next;
+    }
+}
+
 // ---- K2/K3: one ring round ---------------------------------------------------
 // MODE 0: x_next = recv + add            (rounds 1..N-1)
 // MODE 1: x_next = (recv - sub) + add    (rounds N..c-1)
@@ -260,7 +355,7 @@ struct RoundParams {
     int wg_per_worker;
 };
 
-constexpr int kRoundThreads = 128;
+constexpr int kRoundThreads = 256;
 
 template <int MODE, bool VEC>
 __global__ __launch_bounds__(kRoundThreads) void k_round(RoundParams a) {
@@ -308,8 +403,8 @@ struct DecParams {
 template <int KS, bool VEC, bool AREG, bool FAST>
 __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
     extern __shared__ float smem[];
-    const int worker = blockIdx.x / a.wg_per_worker;
-    const int wg = blockIdx.x - worker * a.wg_per_worker;
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int nmt = a.mt1 - a.mt0;
@@ -329,7 +424,7 @@ __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
         stage_fragments(sfrag, gfrag, nmt, KSx);
     }
     // rows K..4 KSx-1 of the last K-step repeat row K-1; their coefficients are zero
-    for (int t = threadIdx.x; t < 4 * KSx; t += kThreads)
+    for (int t = threadIdx.x; t < 4 * KS; t += kThreads)
         srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
     __syncthreads();
     float *out = a.out + (size_t)worker * a.ld_o;
@@ -369,6 +464,63 @@ __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
                 }
             }
         }
+    }
+}
+
+// Pipelined interior decode for c <= 64: same scheme, B rows through the
+// per-worker table of observation slots.
+template <int KS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 20 ? 3 : (KS <= 32 ? 2 : 1)))) void k_decode_pipe(DecParams a) {
+    extern __shared__ float smem[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int MT = a.mt1 - a.mt0;                       // <= kMaxRegTiles
+    const int KSx = a.KSd;
+    constexpr int Q = (KS + 3) / 4;
+    const size_t nfrag = (size_t)MT * Q * 256;
+    float *sfrag = smem;
+    const float **srow = reinterpret_cast<const float **>(smem + nfrag);
+    stage_fragments_padded(sfrag, a.frag + ((size_t)worker * a.MT + a.mt0) * KSx * 64, MT, KSx, KS);
+    // 4 KS row pointers: rows K..4 KS-1 repeat row K-1 (zero coefficients), so
+    // every load below is unconditional
+    for (int t = threadIdx.x; t < 4 * KS; t += kThreads)
+        srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
+    __syncthreads();
+    float *out = a.out + (size_t)worker * a.ld_o;
+    const size_t p = a.sb.p;
+    const size_t stride = (size_t)a.wg_per_worker * kWaves;
+    size_t blk = a.blk0 + (size_t)wg * kWaves + wave;
+    if (blk >= a.blk1) return;
+    v4f b[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load(srow[ks * 4 + krow] + blk * 64 + 4 * col);
+    while (true) {
+        const size_t e0 = blk * 64;
+        v4f acc[kMaxRegTiles][4];
+#pragma unroll
+        for (int mt = 0; mt < kMaxRegTiles; ++mt)
+            if (mt < MT) mtile_mma_lds<KS>(acc[mt], b, sfrag + (size_t)mt * Q * 256, lane);
+        const size_t next = blk + stride;
+        if (next < a.blk1) {
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load(srow[ks * 4 + krow] + next * 64 + 4 * col);
+        }
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+        for (int mt = 0; mt < kMaxRegTiles; ++mt) {
+            if (mt < MT) {
+                const int mtile = (a.mt0 + mt) * 16;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const v4f v = {acc[mt][0][r], acc[mt][1][r], acc[mt][2][r], acc[mt][3][r]};
+                    nt_store_off(out + e0 + (size_t)(mtile + r) * p, lane_out, v);   // 16 | c
+                }
+            }
+        }
+        if (next >= a.blk1) break;
+        blk = next;
     }
 }
 
@@ -520,8 +672,8 @@ SlotBase slot_base(const cerar_plan *plan, const Geometry &g, float *work, size_
 }
 
 int wg_for(size_t nblk) {
-    // 64-position blocks per workgroup pass = 4 (one per wave); ~8 passes each
-    size_t w = (nblk + 4 * 8 - 1) / (4 * 8);
+    // 64-position blocks per workgroup pass = 4 (one per wave); ~4 passes each
+    size_t w = (nblk + 4 * 4 - 1) / (4 * 4);
     if (w < 1) w = 1;
     if (w > 16384) w = 16384;
     return (int)w;
@@ -532,14 +684,32 @@ enum class Path { kFast, kMaskedVec, kScalar };
 
 template <int KS, bool AREG>
 void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
-    if (path == Path::kFast) hipLaunchKernelGGL((k_encode<KS, true, AREG, true>), grid, dim3(kThreads), lds, s, a);
-    else if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_encode<KS, true, AREG, false>), grid, dim3(kThreads), lds, s, a);
+    if constexpr (AREG) {
+        if (path == Path::kFast) {
+            // up to 4 M-tiles: the pipelined kernel, coefficients staged in LDS
+            const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float);
+            hipLaunchKernelGGL((k_encode_pipe<KS>), grid, dim3(kThreads), l, s, a);
+            return;
+        }
+    }
+    if constexpr (!AREG) {
+        if (path == Path::kFast) {
+            hipLaunchKernelGGL((k_encode<KS, true, AREG, true>), grid, dim3(kThreads), lds, s, a);
+            return;
+        }
+    }
+    if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_encode<KS, true, AREG, false>), grid, dim3(kThreads), lds, s, a);
     else hipLaunchKernelGGL((k_encode<KS, false, AREG, false>), grid, dim3(kThreads), lds, s, a);
 }
 
 template <int KS>
 void launch_decode_ks(const DecParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
-    if (path == Path::kFast) hipLaunchKernelGGL((k_decode<KS, true, false, true>), grid, dim3(kThreads), lds, s, a);
+    if (path == Path::kFast && a.mt1 - a.mt0 <= kMaxRegTiles) {
+        const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float) +
+                         (size_t)4 * KS * sizeof(float *);
+        hipLaunchKernelGGL((k_decode_pipe<KS>), grid, dim3(kThreads), l, s, a);
+    }
+    else if (path == Path::kFast) hipLaunchKernelGGL((k_decode<KS, true, false, true>), grid, dim3(kThreads), lds, s, a);
     else if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_decode<KS, true, false, false>), grid, dim3(kThreads), lds, s, a);
     else hipLaunchKernelGGL((k_decode<KS, false, false, false>), grid, dim3(kThreads), lds, s, a);
 }
@@ -686,7 +856,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     const bool vec = g.vec && (ld_out % 4 == 0) && aligned16(out);
     const BlockSplit bs = split_blocks(plan, g.p, d, vec);
     const int N = plan->N, ks = plan->KSd;
-    const size_t rows_bytes = (size_t)4 * ks * sizeof(float *) + 16;
+    const size_t rows_bytes = (size_t)4 * kMaxDecodeKS * sizeof(float *) + 16;
     const int step = mtiles_per_launch(plan->MT, ks, rows_bytes);
     for (int mt0 = 0; mt0 < plan->MT; mt0 += step) {
         a.mt0 = mt0;
@@ -696,6 +866,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
         else if (ks <= 8) decode_ks<8>(a, bs, lds, s, N);
         else if (ks <= 12) decode_ks<12>(a, bs, lds, s, N);
         else if (ks <= 16) decode_ks<16>(a, bs, lds, s, N);
+        else if (ks <= 18) decode_ks<18>(a, bs, lds, s, N);
         else if (ks <= 20) decode_ks<20>(a, bs, lds, s, N);
         else if (ks <= 24) decode_ks<24>(a, bs, lds, s, N);
         else if (ks <= 32) decode_ks<32>(a, bs, lds, s, N);
