@@ -22,6 +22,7 @@ import argparse
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -45,10 +46,188 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = headline)")
     ap.add_argument("--plan-iters", type=int, default=100, help="ALS iterations of the kappa design")
-    ap.add_argument("--cpu-positions", type=int, default=1 << 19,
+    ap.add_argument("--cpu-positions", type=int, default=1 << 21,
                     help="positions of the bounded oracle sample (0 = skip cpu_baseline)")
     ap.add_argument("--copy-floats", type=int, default=1 << 30, help="size of the copy reference")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("TRACE_DIR", "BENCH_LOG", "OUT"),
+                    help="write the summary of a rocprofv3 --kernel-trace --stats run of this bench")
+    ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
+                    help="write the HBM traffic summary of two rocprofv3 --pmc runs of this bench")
     return ap.parse_args()
+
+
+# ---- rocprofv3 summaries ------------------------------------------------------
+
+KERNEL_SOURCES = ("paper_2609_23898_amd/csrc/kernels.hip", "paper_2609_23898_amd/csrc/cerar_internal.hpp")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_cerar_n8_c64_pythia1.4b.txt")
+FAMILIES = (("k_encode", "k_encode (K1)"), ("k_round<0,", "k_round<0> (K2: recv + delta)"),
+            ("k_round<1,", "k_round<1> (K3: recv - delta + delta)"),
+            ("k_round<2,", "k_round<2> (K3: recv - delta)"), ("k_decode", "k_decode (K4)"),
+            ("k_copy4", "k_copy4 (copy reference)"))
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def family_of_name(name):
+    for key, fam in FAMILIES:
+        if re.search(r"\b" + re.escape(key), name):
+            return fam
+    return None
+
+
+def _find_csv(d, suffix):
+    import glob
+    hits = sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True))
+    if not hits:
+        raise SystemExit(f"no *{suffix} under {d}")
+    return hits[-1]
+
+
+def _read_csv(path):
+    import csv
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def _step_bytes_cfg4():
+    """Algorithmic bytes per launch of each family at the Pythia-1.4B workload."""
+    from paper_2609_23898_amd import cerar as C
+    from paper_2609_23898_amd import synth
+    wl = synth.workload(4)
+    N, c = wl.N, wl.c
+    p = -(-wl.d // c)
+    bw = C.phase_bytes_per_worker(N, c, p)
+    return {"k_encode (K1)": N * bw["encode"], "k_decode (K4)": N * bw["decode"],
+            "k_round<0> (K2: recv + delta)": N * bw["rounds"][1],
+            "k_round<1> (K3: recv - delta + delta)": N * bw["rounds"][N],
+            "k_round<2> (K3: recv - delta)": N * bw["rounds"][c]}
+
+
+def summarize_trace(trace_dir, bench_log, out_path):
+    stats = _read_csv(_find_csv(trace_dir, "kernel_stats.csv"))
+    bench = None
+    with open(bench_log) as f:
+        for line in f:
+            if line.startswith("{"):
+                bench = json.loads(line)
+    rows, other = [], [0, 0.0, 0.0]
+    for r in stats:
+        if "cerar::" not in r["Name"]:          # torch and runtime kernels: synthetic inputs, copies
+            other[0] += int(r["Calls"])
+            other[1] += float(r["TotalDurationNs"])
+            other[2] += float(r["Percentage"])
+            continue
+        name = re.sub(r"^(void )?cerar::\(anonymous namespace\)::", "", r["Name"])
+        name = re.sub(r"\(.*$", "", name)
+        rows.append((name, int(r["Calls"]), float(r["TotalDurationNs"]), float(r["AverageNs"]),
+                     float(r["Percentage"])))
+    rows.sort(key=lambda x: -x[2])
+    rows.append(("other kernels (torch input generation, untimed)", other[0], other[1],
+                 other[1] / max(other[0], 1), other[2]))
+    lines = ["# Kernel durations of the headline bench, rocprofv3 kernel trace",
+             "# workload: N=8 workers, c=64, d=1,414,647,808 fp32 (Pythia-1.4B-shaped), kappa_max=1e3 plan",
+             "# command (repo root, MI355X):",
+             "#   rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof/trace -o trace -- python3 bench.py "
+             "> gpurun_out/prof/trace_bench.log",
+             "#   python3 bench.py --summarize-trace gpurun_out/prof/trace gpurun_out/prof/trace_bench.log "
+             "profiles/kernel_trace_cerar_n8_c64_pythia1.4b.txt",
+             f"# kernel_source_sha256: {kernel_source_hash()}", "",
+             f"{'kernel':<60s} {'calls':>6s} {'avg_us':>10s} {'total_ms':>10s} {'pct':>6s}"]
+    fam_ns = {}
+    for name, calls, tot, avg, pct in rows:
+        short = name if len(name) <= 60 else name[:57] + "..."
+        lines.append(f"{short:<60s} {calls:6d} {avg / 1e3:10.1f} {tot / 1e6:10.2f} {pct:6.2f}")
+        fam = family_of_name(name)
+        if fam:
+            t, n = fam_ns.get(fam, (0.0, 0))
+            fam_ns[fam] = (t + tot, n + calls)
+    lines += ["", "# per family: trace average vs the bench's HIP-event average on the launch stream",
+              f"{'family':<42s} {'trace_avg_ms':>12s} {'event_avg_ms':>12s} {'ratio':>7s}"]
+    for fam, (t, n) in fam_ns.items():
+        ev = bench["kernels"].get(fam, {}).get("avg_ms") if bench else None
+        ta = t / n / 1e6
+        lines.append(f"{fam:<42s} {ta:12.4f} {ev if ev is not None else float('nan'):12.4f} "
+                     f"{(ev / ta) if ev else float('nan'):7.3f}")
+    if bench:
+        lines += ["", f"# bench line: {bench['ms_per_step']} ms/step, {bench['value']} GB/s "
+                      f"({bench['config']['pct_hbm_peak']}% of 8 TB/s); roofline kernel "
+                      f"{bench['roofline']['kernel']} at {bench['roofline']['achieved']} GB/s"]
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _pmc_per_family(d, counter):
+    rows = _read_csv(_find_csv(d, "counter_collection.csv"))
+    acc = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        fam = family_of_name(r["Kernel_Name"])
+        if fam is None:
+            continue
+        v, n = acc.get(fam, (0.0, 0))
+        acc[fam] = (v + float(r["Counter_Value"]), n + 1)
+    return {fam: (v / n, n) for fam, (v, n) in acc.items()}
+
+
+def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30):
+    fetch = _pmc_per_family(fetch_dir, "FETCH_SIZE")
+    write = _pmc_per_family(write_dir, "WRITE_SIZE")
+    copy = "k_copy4 (copy reference)"
+    copy_kib = copy_floats * 4 / 1024.0
+    f_scale = fetch[copy][0] / copy_kib
+    w_scale = write[copy][0] / copy_kib
+    algo = _step_bytes_cfg4()
+    lines = ["# HBM traffic per dispatch from rocprofv3 counters (FETCH_SIZE, WRITE_SIZE in KiB per dispatch)",
+             "# workload: N=8 workers, c=64, d=1,414,647,808 fp32 (Pythia-1.4B-shaped), kappa_max=1e3 plan",
+             "# commands (repo root, MI355X), one counter per run:",
+             "#   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
+             "-d gpurun_out/prof/fetch -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
+             "#   rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
+             "-d gpurun_out/prof/write -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
+             "#   python3 bench.py --summarize-pmc gpurun_out/prof/fetch gpurun_out/prof/write "
+             "profiles/hbm_traffic_cerar_n8_c64_pythia1.4b.txt",
+             "# scale: each counter divided by what it reads for the plain copy kernel k_copy4 moving "
+             f"{copy_floats} floats ({copy_kib:.0f} KiB read and written per dispatch)",
+             f"kernel_source_sha256: {kernel_source_hash()}",
+             f"fetch_scale: {f_scale:.5f}", f"write_scale: {w_scale:.5f}", "",
+             f"{'family':<42s} {'n':>4s} {'FETCH_KiB':>14s} {'WRITE_KiB':>14s} {'traffic_B':>16s} "
+             f"{'algorithmic_B':>16s} {'ratio':>7s}"]
+    for fam in [f for _, f in FAMILIES]:
+        if fam not in fetch or fam not in write:
+            continue
+        fk, n = fetch[fam]
+        wk, _ = write[fam]
+        traffic = (fk / f_scale + wk / w_scale) * 1024.0
+        a = algo.get(fam, 2 * copy_floats * 4)
+        lines.append(f"{fam:<42s} {n:4d} {fk:14.1f} {wk:14.1f} {traffic:16.0f} {a:16d} {traffic / a:7.4f}")
+        lines.append(f"traffic_bytes_per_launch[{fam}]: {traffic:.0f}")
+    with open(out_path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def committed_traffic(family):
+    """HBM bytes per launch of `family` from the committed counter summary, or
+    None when there is none or the kernels changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"^kernel_source_sha256: (\w+)", text, re.M)
+    if not m or m.group(1) != kernel_source_hash():
+        return None
+    m = re.search(r"^traffic_bytes_per_launch\[" + re.escape(family) + r"\]: (\d+)", text, re.M)
+    return int(m.group(1)) if m else None
 
 
 def product_plan(C, wl, iters):
@@ -115,6 +294,12 @@ def cpu_baseline(wl, S):
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, copy_floats=args.copy_floats)
+        return
     if args.gpus != 1:
         print(f"bench.py runs the single-GPU simulation of all N workers; --gpus {args.gpus} is not "
               "supported (multi-GPU CERAR is not part of this build)", file=sys.stderr)
@@ -253,7 +438,7 @@ def main():
                    "bytes_per_step": step_bytes, "encode": "out of place (grads kept for every step)"},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
-                     "traffic": None},
+                     "traffic": committed_traffic(dominant)},
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
         "copy_gbps": round(copy_gbps, 1),
