@@ -1,0 +1,130 @@
+"""The seeded input generators: the published splitmix64 sequence, identical
+bits on the NumPy and torch paths, the distributions the workloads ask for,
+and the model shapes and bucket layout of the synthetic gradients."""
+
+import math
+
+import numpy as np
+import pytest
+
+from paper_2609_23898_amd import synth
+
+
+def test_splitmix64_matches_published_sequence():
+    # splitmix64 from state 1234567: the first five outputs of the reference
+    # generator (Steele, Lea & Flood 2014; Vigna's public-domain C version)
+    x = 1234567
+    got = []
+    for _ in range(5):
+        x = (x + synth._GOLDEN) & synth._MASK64
+        got.append(synth._mix64_int(x))
+    assert got == [6457827717110365317, 3203168211198807973, 9817491932198370423,
+                   4593380528125082431, 16408922859458223821]
+
+
+def test_numpy_and_torch_paths_give_identical_bits():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(0)
+    for cfg in (1, 3, 4, 5):
+        wl = synth.workload(cfg)
+        idx = np.unique(np.concatenate([rng.integers(0, wl.d, 20000), [0, wl.d - 1, wl.d, wl.d + 5]]))
+        for w in (0, wl.N - 1):
+            a = wl.values_np(w, idx)
+            b = wl.values_torch(w, torch.from_numpy(idx)).numpy()
+            assert a.dtype == np.float32 and b.dtype == np.float32
+            np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
+    key = synth.stream_key(9, 3)
+    idx = np.arange(5000)
+    np.testing.assert_array_equal(synth.normal_np(key, idx),
+                                  synth.normal_torch(key, torch.from_numpy(idx)).numpy())
+    np.testing.assert_array_equal(synth.uniform32_np(key, idx, 6),
+                                  synth.uniform32_torch(key, torch.from_numpy(idx), 6).numpy())
+
+
+def test_fill_matches_pointwise_values():
+    torch = pytest.importorskip("torch")
+    wl = synth.workload(3)
+    out = torch.empty(10007, dtype=torch.float32)
+    wl.fill_torch(out, 2, start=wl.d - 5000, chunk=4096)
+    ref = wl.values_np(2, np.arange(wl.d - 5000, wl.d - 5000 + 10007))
+    np.testing.assert_array_equal(out.numpy(), ref)
+    assert np.all(ref[5000:] == 0)                     # beyond d: the zero pad
+
+
+def test_irwin_hall_normal_moments():
+    # Irwin-Hall(12) - 6 has mean 0, variance exactly 1, support [-6, 6]
+    x = synth.normal_np(synth.stream_key(1, 1), np.arange(1_000_000))
+    assert abs(x.mean()) < 5e-3
+    assert abs(x.var() - 1.0) < 5e-3
+    assert x.min() >= -6 and x.max() <= 6
+    # fourth moment of IH(12)-6: 3 - 1.2/12 = 2.9
+    assert abs(np.mean(x ** 4) - 2.9) < 0.03
+
+
+def test_workers_are_independent_streams():
+    wl = synth.workload(2)
+    idx = np.arange(200_000)
+    a = wl.values_np(0, idx).astype(np.float64)
+    b = wl.values_np(1, idx).astype(np.float64)
+    assert abs(np.corrcoef(a, b)[0, 1]) < 0.01
+    assert abs(a.std() - 1e-3) < 2e-5                  # N(0, 1e-6)
+
+
+def test_outliers_are_one_percent_at_100x():
+    wl = synth.workload(5)
+    idx = np.arange(400_000)
+    key = wl.worker_key(3)
+    hit = synth.uniform32_np(key, idx, 6) < wl.outlier_threshold
+    assert abs(hit.mean() - 0.01) < 1e-3
+    v = wl.values_np(3, idx).astype(np.float64)
+    base = synth.normal_np(key, idx)
+    np.testing.assert_allclose(v[hit], (base[hit] * 100.0).astype(np.float32), rtol=0)
+    np.testing.assert_allclose(v[~hit], base[~hit].astype(np.float32), rtol=0)
+
+
+def test_model_shapes():
+    g = synth.gpt2_small_tensor_sizes()
+    assert len(g) == 148 and sum(g) == 124_439_808
+    p = synth.pythia_1_4b_tensor_sizes()
+    assert len(p) == 292 and sum(p) == 1_414_647_808
+    assert synth.workload(4).d == 1_414_647_808 and synth.workload(3).d == 124_439_808
+
+
+def test_per_tensor_scales_are_lognormal_and_shared():
+    wl = synth.workload(4)
+    s = wl.tensor_scales().astype(np.float64)
+    z = np.log(s)
+    assert len(s) == 292
+    assert abs(z.mean()) < 0.25 and abs(z.std() - 1.0) < 0.2
+    # the scale applies to a whole tensor: the ratio value / normal is constant inside it
+    off = np.concatenate([[0], np.cumsum(synth.pythia_1_4b_tensor_sizes())])
+    t = 5
+    idx = np.arange(off[t], off[t] + 1000)
+    for w in (0, 7):
+        ratio = wl.values_np(w, idx).astype(np.float64) / synth.normal_np(wl.worker_key(w), idx)
+        np.testing.assert_allclose(ratio, s[t], rtol=1e-6)
+
+
+def test_ddp_buckets_cover_the_gradient():
+    sizes = synth.gpt2_small_tensor_sizes()
+    b = synth.ddp_buckets(sizes)
+    assert len(b) == 17
+    d = sum(sizes)
+    pos = 0
+    offsets = set(np.concatenate([[0], np.cumsum(sizes)]).tolist())
+    for off, ln in b:
+        assert off == pos and ln > 0
+        assert off in offsets and off + ln in offsets      # buckets hold whole tensors
+        pos += ln
+        if ln > synth.DDP_BUCKET_FLOATS:                   # only a single oversize tensor
+            assert ln in sizes
+    assert pos == d
+    assert synth.workload(3).buckets == b
+
+
+def test_base_matrix_is_seeded():
+    a = synth.base_matrix(7, 8, 64)
+    assert a.shape == (8, 64) and a.dtype == np.float64
+    np.testing.assert_array_equal(a, synth.base_matrix(7, 8, 64))
+    assert not np.array_equal(a, synth.base_matrix(8, 8, 64))
+    assert math.isclose(float(np.std(synth.base_matrix(1, 64, 64))), 1.0, rel_tol=0.05)
