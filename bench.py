@@ -237,8 +237,8 @@ def product_plan(C, wl, iters):
         return C.Plan(wl.N, wl.c, "o_eps", 1e-3, seed=1000 + wl.N), "O(eps) eps=1e-3"
     if wl.c == 128:
         return C.Plan(wl.N, wl.c, "o_eps", 1e-2, seed=1000 + wl.N), "O(eps) eps=1e-2"
-    return (C.Plan(wl.N, wl.c, "kappa", 1e3, seed=1000 + wl.N, eps0=0.3, als_iters=iters),
-            f"kappa_max=1e3 ALS {iters} it from O(0.3)")
+    return (C.Plan(wl.N, wl.c, "kappa", 1e3, seed=1000 + wl.N, eps0=0.3, als_iters=iters, als_order=1),
+            f"kappa_max=1e3 ALS {iters} it (projection before each R-step) from O(0.3)")
 
 
 def family_of(k, N, c, L):
@@ -273,7 +273,7 @@ def cpu_baseline(wl, S):
     with threadpool_limits(limits=1):
         if wl.c == 64 or wl.c == 32:
             B = synth.base_matrix(1000 + N, N, c)
-            U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(c)), 0.3, 1e3, 20)
+            U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(c)), 0.3, 1e3, 20, order="projected")
             plan_desc = "oracle kappa design (20 ALS iterations)"
         else:
             B = synth.base_matrix(1000 + N, N, c)

@@ -75,7 +75,13 @@ typedef struct {
     const double *perturb;  /* optional host c x c row-major H (O_EPS, KAPPA); default diag(nodes) */
     const double *nodes;    /* optional host c distinct reals xi; default cos((2j-1) pi / 2c) */
     double eps0;            /* KAPPA: eps of the O(eps) starting plan; <= 0 selects 0.3 */
-    int als_iters;          /* KAPPA: ALS iterations (U-step, R-step, projection); <= 0 selects 100 */
+    int als_iters;          /* KAPPA: ALS iterations; <= 0 selects 100 */
+    int als_order;          /* KAPPA: steps of one iteration.  0: U-step, R-step, then the
+                             * projection (the order Sec. II-D states; the next U-step
+                             * overwrites the projected U, so only the last projection acts).
+                             * 1: U-step, projection, R-step, so every R-step fits a projected
+                             * U (about half the Phi at N=8, c=32..64).  Both end with a
+                             * projection and an R-step, so kappa_2(M_i) <= kappa_max holds. */
 } cerar_plan_desc;
 
 /* Plan diagnostics (host fp64). */

@@ -235,17 +235,28 @@ def project_singular_values(U, kappa_max):
     return P @ (s[:, :, None] * QT), (a0, b0)
 
 
-def kappa_design(B, H, eps0, kappa_max, iters):
+def kappa_design(B, H, eps0, kappa_max, iters, order="paper"):
     """Alternating least squares for eq. (16), started from the O(eps) plan
-    with D = I + eps0 H (Sec. II-D).  Returns (U, R)."""
+    with D = I + eps0 H (Sec. II-D).  Returns (U, R).
+
+    order "paper": each iteration minimises Phi over U (R fixed), then over R
+    (U fixed), then projects the singular values of every U_k, as Sec. II-D
+    states; a last R-step fits the decoders to the projected encoders.
+    order "projected": U-step, projection, R-step, so that every R-step fits
+    projected encoders (a variant, not the paper's stated order)."""
     B = np.asarray(B, dtype=np.float64)
     N, c = B.shape
     U, R = mpc_plan(B, o_eps_perturbation(H, eps0))
     for _ in range(iters):
         U = u_step(R, N, c)
+        if order == "paper":
+            R = r_step(U)
+            U, _ = project_singular_values(U, kappa_max)
+        else:
+            U, _ = project_singular_values(U, kappa_max)
+            R = r_step(U)
+    if order == "paper":
         R = r_step(U)
-        U, _ = project_singular_values(U, kappa_max)
-    R = r_step(U)
     return U, R
 
 

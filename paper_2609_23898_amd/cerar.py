@@ -34,7 +34,7 @@ class PlanDesc(ctypes.Structure):
                 ("base", ctypes.POINTER(ctypes.c_double)),
                 ("perturb", ctypes.POINTER(ctypes.c_double)),
                 ("nodes", ctypes.POINTER(ctypes.c_double)),
-                ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int)]
+                ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int), ("als_order", ctypes.c_int)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -131,7 +131,7 @@ class Plan:
     """Encoding/decoding plan (host fp64), see cerar_plan_create_desc."""
 
     def __init__(self, N, c, kind, param=0.0, seed=0, base=None, perturb=None, nodes=None,
-                 eps0=0.0, als_iters=0, _handle=None):
+                 eps0=0.0, als_iters=0, als_order=0, _handle=None):
         L = lib()
         self._h = _P()
         if _handle is not None:
@@ -149,7 +149,8 @@ class Plan:
 
             kind = _KINDS[kind] if isinstance(kind, str) else int(kind)
             desc = PlanDesc(N, c, kind, float(param), int(seed), arr(base, N * c),
-                            arr(perturb, c * c), arr(nodes, c), float(eps0), int(als_iters))
+                            arr(perturb, c * c), arr(nodes, c), float(eps0), int(als_iters),
+                            int(als_order))
             _check(L.cerar_plan_create_desc(ctypes.byref(desc), ctypes.byref(self._h)))
         info = self.info()
         self.N, self.c, self.L = info["N"], info["c"], info["L"]

@@ -306,6 +306,8 @@ int validate(const cerar_plan_desc *d) {
             if (d->param < std::sqrt((double)d->N))
                 return fail(CERAR_E_INVAL, "kappa_max=%g below sqrt(N)=%g: the projection interval would be empty",
                             d->param, std::sqrt((double)d->N));
+            if (d->als_order != 0 && d->als_order != 1)
+                return fail(CERAR_E_INVAL, "als_order=%d must be 0 or 1", d->als_order);
             break;
         default:
             return fail(CERAR_E_INVAL, "unknown construction %d", (int)d->kind);
@@ -516,12 +518,20 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
             p->info.phi_initial = phi_of(p, p->U, p->R);
             const int iters = desc->als_iters > 0 ? desc->als_iters : 100;
             double a0 = kNaN, b0 = kNaN;
+            const bool project_first = desc->als_order == 1;
             for (int it = 0; it < iters && result == CERAR_OK; ++it) {
-                if (!u_step(p, p->R, p->U)) result = fail(CERAR_E_SINGULAR, "U-step normal equations singular");
-                else if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
-                else project(p, p->U, desc->param, a0, b0);
+                if (!u_step(p, p->R, p->U)) {
+                    result = fail(CERAR_E_SINGULAR, "U-step normal equations singular");
+                } else if (project_first) {             // U-step, projection, R-step
+                    project(p, p->U, desc->param, a0, b0);
+                    if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
+                } else {                                // U-step, R-step, projection (Sec. II-D)
+                    if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
+                    else project(p, p->U, desc->param, a0, b0);
+                }
             }
-            if (result == CERAR_OK && !r_step(p, p->U, p->R))
+            // the decoders of the final (projected) encoders
+            if (result == CERAR_OK && !project_first && !r_step(p, p->U, p->R))
                 result = fail(CERAR_E_SINGULAR, "final R-step rank deficient");
             p->info.proj_a0 = a0;
             p->info.proj_b0 = b0;

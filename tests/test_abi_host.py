@@ -92,14 +92,17 @@ def test_exact_plan_phi_zero():
 
 
 @pytest.mark.parametrize("N,c,iters", [(4, 6, 8), (4, 9, 15), (8, 16, 10)])
-def test_kappa_design_matches_oracle_iterates(N, c, iters):
-    """Same steps (U-step, R-step, projection) from the same start give the same
-    iterates in both implementations; kappa_2(M_i) <= kappa_max holds."""
+@pytest.mark.parametrize("order", [0, 1])
+def test_kappa_design_matches_oracle_iterates(N, c, iters, order):
+    """Same steps (U-step, R-step, projection in either order) from the same
+    start give the same iterates in both implementations; kappa_2(M_i) <=
+    kappa_max holds."""
     B = synth.base_matrix(11, N, c)
     kmax = 1e3
-    plan = C.Plan(N, c, "kappa", kmax, base=B, eps0=0.3, als_iters=iters)
+    plan = C.Plan(N, c, "kappa", kmax, base=B, eps0=0.3, als_iters=iters, als_order=order)
     U, R = plan.matrices()
-    Uo, Ro = P.kappa_design(B, np.diag(P.chebyshev_nodes(c)), 0.3, kmax, iters)
+    Uo, Ro = P.kappa_design(B, np.diag(P.chebyshev_nodes(c)), 0.3, kmax, iters,
+                            order="paper" if order == 0 else "projected")
     np.testing.assert_allclose(U, Uo, rtol=0, atol=1e-7 * np.abs(Uo).max())
     np.testing.assert_allclose(R, Ro, rtol=0, atol=1e-7 * np.abs(Ro).max())
     info = plan.info()
@@ -139,6 +142,12 @@ def test_explicit_plan_roundtrip():
 def test_invalid_plan_arguments(args):
     with pytest.raises(C.CerarError) as ei:
         C.Plan(*args)
+    assert ei.value.status == -1
+
+
+def test_invalid_als_order():
+    with pytest.raises(C.CerarError) as ei:
+        C.Plan(4, 5, "kappa", 1e3, seed=1, als_order=2)
     assert ei.value.status == -1
 
 

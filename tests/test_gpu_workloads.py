@@ -143,7 +143,7 @@ def test_workload3_gpt2_buckets():
     torch, dev = torch_dev()
     wl = synth.workload(3)
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
-    U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(wl.c)), 0.3, 1e3, 20)
+    U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(wl.c)), 0.3, 1e3, 20, order="projected")
     kappa = OP.max_kappa_M(U)
     assert kappa <= 1e3
     plan = C.Plan.explicit(U, R)
@@ -167,7 +167,7 @@ def test_workload4_pythia_headline():
     torch, dev = torch_dev()
     wl = synth.workload(4)
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
-    U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(wl.c)), 0.3, 1e3, 20)
+    U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(wl.c)), 0.3, 1e3, 20, order="projected")
     kappa = OP.max_kappa_M(U)
     assert kappa <= 1e3
     plan = C.Plan.explicit(U, R)

@@ -251,15 +251,33 @@ def test_projection_bounds_kappa_of_every_M():
         assert P.max_kappa_M(Up) <= kmax * (1 + 1e-9)
 
 
-def test_kappa_design_is_feasible_and_better_than_zero_plan():
+@pytest.mark.parametrize("order", ["paper", "projected"])
+def test_kappa_design_is_feasible_and_better_than_zero_plan(order):
     rng = np.random.default_rng(9)
     for N, c in [(4, 4), (4, 9), (8, 16)]:
         B = rand_base(rng, N, c)
-        U, R = P.kappa_design(B, np.diag(P.chebyshev_nodes(c)), 0.3, 1e3, 30)
+        U, R = P.kappa_design(B, np.diag(P.chebyshev_nodes(c)), 0.3, 1e3, 30, order=order)
         assert P.max_kappa_M(U) <= 1e3 * (1 + 1e-9)
         # Phi of the trivial decoder R = 0 is ||T||^2 per worker = N * N c
         assert 0 < P.phi(U, R) < N * N * c
+        # the returned decoders are the least-squares ones for the returned encoders
         np.testing.assert_allclose(R, P.r_step(U), atol=1e-10)
+        # and the encoders lie in the projected set (Sec. II-D)
+        s = np.linalg.svd(U, compute_uv=False)
+        assert s.max() / s.min() <= 1e3 / np.sqrt(N) * (1 + 1e-9)
+
+
+def test_kappa_design_orders_share_their_first_u_step():
+    """Both orders start from the same O(eps0) plan and the same U-step; with
+    one iteration they differ only in whether the R-step saw the projection,
+    and the final R-step makes them identical."""
+    rng = np.random.default_rng(10)
+    B = rand_base(rng, 4, 9)
+    H = np.diag(P.chebyshev_nodes(9))
+    Ua, Ra = P.kappa_design(B, H, 0.3, 1e3, 1, order="paper")
+    Ub, Rb = P.kappa_design(B, H, 0.3, 1e3, 1, order="projected")
+    np.testing.assert_allclose(Ua, Ub, atol=1e-12)
+    np.testing.assert_allclose(Ra, Rb, atol=1e-10)
 
 
 def test_vandermonde_base_rows_are_node_powers():
