@@ -157,6 +157,66 @@ def test_ring_simulate_parity(name, N, c, d, kind, param):
         assert err_orc < 1e-12 and err_gpu < 1e-5        # exact ring all-reduce (c = N)
 
 
+EDGE = [
+    # name, N, c, d: degenerate and extreme shapes
+    ("d1", 4, 8, 1),                       # p = 1: seven chunks are pure padding
+    ("d-below-c", 4, 8, 7),
+    ("N2-c2-exact", 2, 2, 2 * 1000 + 1),   # c = N, the textbook ring
+    ("N2-c128", 2, 128, 128 * 70 + 5),     # largest c, smallest N
+    ("N64-c64-exact", 64, 64, 64 * 80),    # largest N
+    ("N64-c65", 64, 65, 65 * 64 + 1),
+    ("p-63", 4, 16, 16 * 63),              # one partial 64-position block
+    ("p-64", 4, 16, 16 * 64),              # exactly one block
+    ("p-65", 4, 16, 16 * 65),
+]
+
+
+@pytest.mark.parametrize("name,N,c,d", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_shapes(name, N, c, d):
+    """Well-conditioned explicit plans (orthogonal encoders, least-squares
+    decoders; for c = N the exact plan with B = I) on degenerate shapes."""
+    if c == N:
+        U, R = OP.mpc_plan(np.eye(N), np.eye(N))       # B = I: the textbook ring schedule
+    else:
+        U, R = orthogonal_plan(N, c, seed=N + c)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=c + d)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    sync()
+    gpu = out.double().cpu().numpy()
+    ref = OR.allreduce(g, U, R)
+    assert np.all(np.isfinite(gpu))
+    assert max_rel_l2(gpu, ref) <= 1e-4, name
+    if c == N:
+        S = OR.exact_sum(g)
+        assert max(rel_l2(gpu[i], S) for i in range(N)) < 1e-5
+
+
+def test_side_stream_and_step_calls_match_single_call():
+    """The step-wise calls on a non-default stream give the same bits as the
+    single call on the current stream (same kernels, ordered by the stream)."""
+    torch, dev = torch_dev()
+    N, c, d = 8, 64, 64 * 700 + 13
+    U, R = orthogonal_plan(N, c, seed=21)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=21)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    sync()
+    side = torch.cuda.Stream()
+    work2, ws2, out2 = buffers(plan, d)
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for k in range(plan.L + 1):
+            C.encode_round(plan, k, d, grads, work2, ws2, stream=side)
+        C.decode(plan, d, work2, ws2, out2, stream=side)
+    side.synchronize()
+    assert bool(torch.equal(out, out2))
+
+
 def test_in_place_encode_matches_out_of_place():
     N, c, d = 4, 16, 16 * 1000
     U, R = mpc_plan(N, c, 0.3, seed=9)

@@ -218,3 +218,21 @@ def test_workload5_heavy_tail_n16_c128():
           f"closed form: gpu {dev_gpu:.3g}, fp64 oracle {dev_orc:.3g}; closed-form error vs the "
           f"exact sum {err_closed:.4g}", flush=True)
     assert err_closed < 0.1                            # the plan itself is accurate (Prop. 2)
+
+
+def test_chunks_longer_than_the_fast_path_offsets():
+    """N=2, c=64, d=2^32: p = 2^26 floats per chunk, so 12 p floats of lane
+    offsets no longer fit 31 bits and every block takes the masked path with
+    64-bit indexing (the largest chunk length the workloads come near)."""
+    torch, dev = torch_dev()
+    wl = synth.Workload("N=2 c=64 d=2^32 iid N(0,1)", 2, 64, 1 << 32, seed=6)
+    U, R = orthogonal_plan(wl.N, wl.c, seed=66)
+    kappa = OP.max_kappa_M(U)
+    plan = C.Plan.explicit(U, R)
+    p = -(-wl.d // wl.c)
+    assert (12 * p + 64) * 4 >= 1 << 31
+    grads = device_grads(wl, torch, dev)
+    work, ws, out = C.allocate(plan, wl.d, dev)
+    run_stepwise(plan, wl.d, grads, work, ws, out)
+    torch.cuda.synchronize()
+    check_sampled("2^32 floats per worker", wl, U, R, grads, out, sample_positions(p, 8192, 6), kappa)
