@@ -202,6 +202,20 @@ class Plan:
                                                     ctypes.byref(wf), ctypes.byref(wb)))
         return wf.value, wb.value
 
+    def save(self, path):
+        """Write the plan's fp64 matrices to an .npz file (plans are built
+        offline once; Plan.load rebuilds the same plan as an explicit one)."""
+        U, R = self.matrices()
+        info = self.info()
+        np.savez(path, U=U, R=R, kind=np.int32(info["kind"]), param=np.float64(info["param"]),
+                 seed_used=np.uint64(info["seed_used"]))
+
+    @classmethod
+    def load(cls, path):
+        """Plan from a file written by save()."""
+        with np.load(path, allow_pickle=False) as z:
+            return cls.explicit(z["U"], z["R"])
+
     def close(self):
         if self._h:
             lib().cerar_plan_destroy(self._h)

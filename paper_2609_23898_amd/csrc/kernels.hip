@@ -23,6 +23,15 @@ namespace cerar {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+// Loads through a pointer the compiler cannot place (one read from LDS, as
+// the decode's row table) would be flat loads, which count against the LDS
+// wait counter too and so serialise the table reads with the data loads.
+// Every buffer here is global memory: say so.
+typedef __attribute__((address_space(1))) const v4f global_cv4f;
+typedef __attribute__((address_space(1))) const float global_cf;
+__device__ inline v4f nt_load_g(const float *ptr) { return __builtin_nontemporal_load((global_cv4f *)(ptr)); }
+__device__ inline v4f load_g(const float *ptr) { return *(global_cv4f *)(ptr); }
+__device__ inline float load1_g(const float *ptr) { return *(global_cf *)(ptr); }
 
 constexpr int kThreads = 256;                  // 4 wavefronts of 64
 constexpr int kWaves = kThreads / 64;
@@ -60,18 +69,18 @@ __device__ inline v4f load_tile(const float *__restrict__ row, size_t row_off, s
         if (pos < p) {
             const size_t flat = row_off + pos;
             if (flat + 3 < limit) {
-                v = *reinterpret_cast<const v4f *>(row + pos);
+                v = load_g(row + pos);
             } else {
 #pragma unroll
                 for (int t = 0; t < 4; ++t)
-                    if (flat + t < limit) v[t] = row[pos + t];
+                    if (flat + t < limit) v[t] = load1_g(row + pos + t);
             }
         }
     } else {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const size_t pos = e0 + 16 * (size_t)t + col;
-            if (pos < p && row_off + pos < limit) v[t] = row[pos];
+            if (pos < p && row_off + pos < limit) v[t] = load1_g(row + pos);
         }
     }
     return v;
@@ -443,7 +452,7 @@ __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
             const size_t off = e0 + 4 * (size_t)col;
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks)
-                b[ks] = ks < KSx ? nt_load(srow[ks * 4 + krow] + off) : v4f{0.f, 0.f, 0.f, 0.f};
+                b[ks] = ks < KSx ? nt_load_g(srow[ks * 4 + krow] + off) : v4f{0.f, 0.f, 0.f, 0.f};
         } else {
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
@@ -502,7 +511,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 
     if (blk >= end) return;
     v4f b[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load(srow[ks * 4 + krow] + blk * 64 + 4 * col);
+    for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_g(srow[ks * 4 + krow] + blk * 64 + 4 * col);
     while (true) {
         const size_t e0 = blk * 64;
         v4f acc[kMaxRegTiles][4];
@@ -512,7 +521,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 
         const size_t next = blk + kWaves;
         if (next < end) {
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load(srow[ks * 4 + krow] + next * 64 + 4 * col);
+            for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_g(srow[ks * 4 + krow] + next * 64 + 4 * col);
         }
         const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll

@@ -121,6 +121,19 @@ def test_seeded_plan_is_deterministic_and_gaussian_like():
     assert not np.array_equal(a.matrices()[0], c.matrices()[0])
 
 
+def test_plan_save_and_load(tmp_path):
+    plan = C.Plan(8, 32, "kappa", 1e3, seed=5, als_iters=5, als_order=1)
+    path = tmp_path / "plan.npz"
+    plan.save(path)
+    again = C.Plan.load(path)
+    U, R = plan.matrices()
+    U2, R2 = again.matrices()
+    np.testing.assert_array_equal(U, U2)
+    np.testing.assert_array_equal(R, R2)
+    assert again.info()["phi"] == pytest.approx(plan.info()["phi"], rel=1e-12)
+    assert again.info()["kappa_M"] == pytest.approx(plan.info()["kappa_M"], rel=1e-9)
+
+
 def test_explicit_plan_roundtrip():
     rng = np.random.default_rng(0)
     N, c = 3, 5
