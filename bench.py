@@ -102,7 +102,7 @@ def _step_bytes_cfg4():
     from paper_2609_23898_amd import synth
     wl = synth.workload(4)
     N, c = wl.N, wl.c
-    p = -(-wl.d // c)
+    p = -(-wl.d // c)                            # a multiple of 32 here: the library's p too
     bw = C.phase_bytes_per_worker(N, c, p)
     return {"k_encode (K1)": N * bw["encode"], "k_decode (K4)": N * bw["decode"],
             "k_round<0> (K2: recv + delta)": N * bw["rounds"][1],
@@ -261,7 +261,7 @@ def cpu_baseline(wl, S):
     from paper_2609_23898_amd import synth
 
     N, c, d = wl.N, wl.c, wl.d
-    p = -(-d // c)
+    p = OR.chunk_len(d, c, 32)                   # the library's chunk length (cerar_chunk_len)
     rng = np.random.default_rng(12345)
     pos = np.unique(np.concatenate([rng.integers(0, p, size=S - 1), [p - 1]]))
     S = pos.size

@@ -5,7 +5,8 @@
  * Distributed Training via Ring-Based Coded Approximate All-Reduce").
  *
  * The method (Sec. II): each of N workers splits its length-d gradient into
- * c chunks of p = ceil(d/c) floats (zero pad), encodes them linearly
+ * c chunks of p floats (zero pad; p = ceil(d/c) rounded up to a multiple of
+ * 32, see cerar_chunk_len), encodes them linearly
  * (Delta_i = G_i U_i), runs L = c + N - 2 combine-and-forward rounds on a ring
  * (Algorithm 1, update equations (2)), and decodes its L+1 stored
  * observations linearly (g_hat_i = Y_i R_i) into an approximation of the sum
@@ -129,8 +130,13 @@ int cerar_plan_get_info(const cerar_plan *plan, cerar_plan_info *info);
  * cerar_plan_create_explicit (N*c*c and N*(L+1)*c doubles). Either may be NULL. */
 int cerar_plan_get_matrices(const cerar_plan *plan, double *U, double *R);
 
-/* Geometry for gradient length d: p = ceil(d/c) (message length, Sec. II)
- * and the stride of pool slots in the workspace (p rounded up to 64). */
+/* Geometry for gradient length d: the chunk and message length p (Sec. II:
+ * the gradient is zero-padded to c chunks of p entries, chunk l being entries
+ * [l p, (l+1) p)).  p = ceil(d/c) rounded up to a multiple of 32 floats, so
+ * that every chunk row starts on a 128-byte line; the extra entries are part
+ * of the zero pad of the last chunk, and the output keeps only the first d.
+ * pool_stride is the stride of pool slots in the workspace (p rounded up to
+ * 64).  Errors: E_INVAL (NULL pointers, d == 0). */
 int cerar_chunk_len(const cerar_plan *plan, size_t d, size_t *p, size_t *pool_stride);
 
 /* Device workspace needed for gradient length d: the pool of N*N message
@@ -187,7 +193,7 @@ int cerar_ring_simulate(const cerar_plan *plan, size_t d,
 /* Bucketed all-reduce (one independent CERAR instance per bucket, the same
  * plan for all): bucket b covers flat entries [bucket_off[b],
  * bucket_off[b] + bucket_len[b]) of every worker's gradient and gets its own
- * p_b = ceil(bucket_len[b]/c).  work holds, per worker, the buckets' c*p_b
+ * p_b (cerar_chunk_len of bucket_len[b]).  work holds, per worker, the buckets' c*p_b
  * slots back to back (stride ld_work >= sum_b c*p_b); ws is
  * cerar_bucketed_workspace_bytes.  The buckets run one after another on
  * `stream`, each as its own encode, round and decode launches (all workers

@@ -13,9 +13,14 @@ positions only.
 import numpy as np
 
 
-def chunk_len(d, c):
-    """p = ceil(d / c): the gradient is zero-padded until c divides it (Sec. II)."""
-    return -(-d // c)
+def chunk_len(d, c, align=1):
+    """Chunk (message) length p.  The gradient is zero-padded until it splits
+    into c chunks of p entries (Sec. II); the padding only has to make
+    c p >= d, so p = ceil(d / c) is the least choice (align = 1) and any larger
+    p works the same way.  With align > 1, p is ceil(d / c) rounded up to a
+    multiple of align."""
+    p = -(-d // c)
+    return -(-p // align) * align
 
 
 def exact_sum(grads):
@@ -24,12 +29,12 @@ def exact_sum(grads):
     return np.sum(np.asarray(grads, dtype=np.float64), axis=0)
 
 
-def to_chunks(g, c):
+def to_chunks(g, c, align=1):
     """G_i = [g[0] .. g[c-1]] in R^{p x c}, column l = g[l p:(l+1) p], with the
-    tail beyond d set to zero (Sec. II)."""
+    tail beyond d set to zero (Sec. II); p = chunk_len(d, c, align)."""
     g = np.asarray(g, dtype=np.float64).ravel()
     d = g.size
-    p = chunk_len(d, c)
+    p = chunk_len(d, c, align)
     padded = np.zeros(c * p)
     padded[:d] = g
     return padded.reshape(c, p).T
@@ -128,12 +133,13 @@ def allreduce_chunks(G_list, U, R):
     return [decode(Y[i], R[i]) for i in range(len(G_list))]
 
 
-def allreduce(grads, U, R):
-    """Full pipeline on length-d gradients (N x d); returns g_hat (N x d)."""
+def allreduce(grads, U, R, align=1):
+    """Full pipeline on length-d gradients (N x d); returns g_hat (N x d).
+    `align` sets the chunk length (chunk_len)."""
     grads = np.asarray(grads)
     N, d = grads.shape
     c = U.shape[1]
-    G_list = [to_chunks(grads[i], c) for i in range(N)]
+    G_list = [to_chunks(grads[i], c, align) for i in range(N)]
     ghat = allreduce_chunks(G_list, U, R)
     return np.stack([from_chunks(ghat[i], d) for i in range(N)])
 

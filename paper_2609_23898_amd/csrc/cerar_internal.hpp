@@ -22,6 +22,10 @@ constexpr int kLanes = 64;
 
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// Chunk length p is ceil(d/c) rounded up to a multiple of this many floats
+// (128 bytes); the zero padding of the last chunk absorbs the difference.
+constexpr size_t kChunkAlign = 32;
+
 // One round's per-worker slot operands: next message dst = recv - sub + add
 // (sub/add = -1 when absent; dst = -1 when the round only relabels).
 struct RoundOp {

@@ -301,14 +301,14 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
 // stay in LDS, all M-tile accumulators stay in AGPRs, and the next block's
 // loads are issued before the current block's stores, so every wave keeps
 // loads in flight while its stores drain.
-template <int KS>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 16 ? 3 : 2))) void k_encode_pipe(EncParams a) {
+template <int KS, int MTMAX, int NB>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_encode_pipe(EncParams a) {
     extern __shared__ float sfrag[];
     const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
     const int wg = blockIdx.x / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
-    const int MT = a.mt1 - a.mt0;                       // <= kMaxRegTiles
+    const int MT = a.mt1 - a.mt0;                       // <= MTMAX
     const int KSx = a.KSe;
     constexpr int Q = (KS + 3) / 4;
     stage_fragments_padded(sfrag, a.frag + ((size_t)worker * a.MT + a.mt0) * KSx * 64, MT, KSx, KS);
@@ -318,36 +318,45 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 
     float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
     const size_t p = a.sb.p;
     const size_t first = a.blk0 + (size_t)wg * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
-    size_t blk = first + wave;
+    // each wave takes groups of NB adjacent blocks; a group cut by `end`
+    // re-reads the last block for its missing members and skips their stores
+    size_t blk = first + (size_t)wave * NB;
     if (blk >= end) return;
-    v4f b[KS];
-    {
+    v4f b[NB][KS];
+    auto load_group = [&](size_t g) {
         const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) b[ks] = load_off(src + blk * 64 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
-    }
-    while (true) {
-        const size_t e0 = blk * 64;
-        v4f acc[kMaxRegTiles][4];
+        for (int nb = 0; nb < NB; ++nb) {
+            const size_t bq = min(g + nb, end - 1);
 #pragma unroll
-        for (int mt = 0; mt < kMaxRegTiles; ++mt)
-            if (mt < MT) mtile_mma_lds<KS>(acc[mt], b, sfrag + (size_t)mt * Q * 256, lane);
-        const size_t next = blk + kWaves;
-        if (next < end) {
-            const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) b[ks] = load_off(src + next * 64 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+            for (int ks = 0; ks < KS; ++ks) b[nb][ks] = load_off(src + bq * 64 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
         }
+    };
+    load_group(blk);
+    while (true) {
+        v4f acc[NB][MTMAX][4];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int mt = 0; mt < MTMAX; ++mt)
+                if (mt < MT) mtile_mma_lds<KS>(acc[nb][mt], b[nb], sfrag + (size_t)mt * Q * 256, lane);
+        const size_t next = blk + (size_t)kWaves * NB;
+        if (next < end) load_group(next);
         const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
-        for (int mt = 0; mt < kMaxRegTiles; ++mt) {
-            if (mt < MT) {
-                const int jt = (a.mt0 + mt) * 16;
+        for (int nb = 0; nb < NB; ++nb) {
+            if (blk + nb >= end) break;
+            const size_t e0 = (blk + nb) * 64;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const v4f v = {acc[mt][0][r], acc[mt][1][r], acc[mt][2][r], acc[mt][3][r]};
-                    nt_store_off(dst + e0 + (size_t)(jt + r) * p, lane_out, v);   // 16 | c
-                    if (jt + krow * 4 + r == 0) nt_store_off(x1 + e0, (uint32_t)(4 * col * sizeof(float)), v);
+            for (int mt = 0; mt < MTMAX; ++mt) {
+                if (mt < MT) {
+                    const int jt = (a.mt0 + mt) * 16;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const v4f v = {acc[nb][mt][0][r], acc[nb][mt][1][r], acc[nb][mt][2][r], acc[nb][mt][3][r]};
+                        nt_store_off(dst + e0 + (size_t)(jt + r) * p, lane_out, v);   // 16 | c
+                        if (jt + krow * 4 + r == 0) nt_store_off(x1 + e0, (uint32_t)(4 * col * sizeof(float)), v);
+                    }
                 }
             }
         }
@@ -484,15 +493,16 @@ __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
 }
 
 // Pipelined interior decode for c <= 64: same scheme, B rows through the
-// per-worker table of observation slots.
-template <int KS>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 20 ? 3 : (KS <= 32 ? 2 : 1)))) void k_decode_pipe(DecParams a) {
+// per-worker table of observation slots; NB adjacent blocks per wave when
+// the M-tiles are few (MTMAX <= 2), as in the encode.
+template <int KS, int MTMAX, int NB>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * NB <= 20 ? 3 : (KS * NB <= 32 ? 2 : 1)))) void k_decode_pipe(DecParams a) {
     extern __shared__ float smem[];
     const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
     const int wg = blockIdx.x / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
-    const int MT = a.mt1 - a.mt0;                       // <= kMaxRegTiles
+    const int MT = a.mt1 - a.mt0;                       // <= MTMAX
     const int KSx = a.KSd;
     constexpr int Q = (KS + 3) / 4;
     const size_t nfrag = (size_t)MT * Q * 256;
@@ -507,31 +517,41 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS <= 
     float *out = a.out + (size_t)worker * a.ld_o;
     const size_t p = a.sb.p;
     const size_t first = a.blk0 + (size_t)wg * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
-    size_t blk = first + wave;
+    size_t blk = first + (size_t)wave * NB;
     if (blk >= end) return;
-    v4f b[KS];
+    v4f b[NB][KS];
+    auto load_group = [&](size_t g) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_g(srow[ks * 4 + krow] + blk * 64 + 4 * col);
-    while (true) {
-        const size_t e0 = blk * 64;
-        v4f acc[kMaxRegTiles][4];
+        for (int nb = 0; nb < NB; ++nb) {
+            const size_t off = min(g + nb, end - 1) * 64 + 4 * col;
 #pragma unroll
-        for (int mt = 0; mt < kMaxRegTiles; ++mt)
-            if (mt < MT) mtile_mma_lds<KS>(acc[mt], b, sfrag + (size_t)mt * Q * 256, lane);
-        const size_t next = blk + kWaves;
-        if (next < end) {
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_g(srow[ks * 4 + krow] + next * 64 + 4 * col);
+            for (int ks = 0; ks < KS; ++ks) b[nb][ks] = nt_load_g(srow[ks * 4 + krow] + off);
         }
+    };
+    load_group(blk);
+    while (true) {
+        v4f acc[NB][MTMAX][4];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int mt = 0; mt < MTMAX; ++mt)
+                if (mt < MT) mtile_mma_lds<KS>(acc[nb][mt], b[nb], sfrag + (size_t)mt * Q * 256, lane);
+        const size_t next = blk + (size_t)kWaves * NB;
+        if (next < end) load_group(next);
         const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
-        for (int mt = 0; mt < kMaxRegTiles; ++mt) {
-            if (mt < MT) {
-                const int mtile = (a.mt0 + mt) * 16;
+        for (int nb = 0; nb < NB; ++nb) {
+            if (blk + nb >= end) break;
+            const size_t e0 = (blk + nb) * 64;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const v4f v = {acc[mt][0][r], acc[mt][1][r], acc[mt][2][r], acc[mt][3][r]};
-                    nt_store_off(out + e0 + (size_t)(mtile + r) * p, lane_out, v);   // 16 | c
+            for (int mt = 0; mt < MTMAX; ++mt) {
+                if (mt < MT) {
+                    const int mtile = (a.mt0 + mt) * 16;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const v4f v = {acc[nb][mt][0][r], acc[nb][mt][1][r], acc[nb][mt][2][r], acc[nb][mt][3][r]};
+                        nt_store_off(out + e0 + (size_t)(mtile + r) * p, lane_out, v);   // 16 | c
+                    }
                 }
             }
         }
@@ -704,11 +724,14 @@ enum class Path { kFast, kMaskedVec, kScalar };
 
 template <int KS, bool AREG>
 void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
-    if constexpr (AREG) {
+    if constexpr (AREG && KS >= 4) {
         if (path == Path::kFast) {
-            // up to 4 M-tiles: the pipelined kernel, coefficients staged in LDS
+            // up to 4 M-tiles: the pipelined kernel, coefficients staged in LDS;
+            // NB blocks per wave keep ~16 KB of loads in flight per wave at any c
+            constexpr int MTMAX = KS <= 4 ? 1 : (KS <= 8 ? 2 : 4);
+            constexpr int NB = KS <= 4 ? 4 : (KS <= 8 ? 2 : 1);
             const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float);
-            hipLaunchKernelGGL((k_encode_pipe<KS>), grid, dim3(kThreads), l, s, a);
+            hipLaunchKernelGGL((k_encode_pipe<KS, MTMAX, NB>), grid, dim3(kThreads), l, s, a);
             return;
         }
     }
@@ -727,7 +750,13 @@ void launch_decode_ks(const DecParams &a, Path path, size_t lds, hipStream_t s, 
     if (path == Path::kFast && a.mt1 - a.mt0 <= kMaxRegTiles) {
         const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float) +
                          (size_t)4 * KS * sizeof(float *);
-        hipLaunchKernelGGL((k_decode_pipe<KS>), grid, dim3(kThreads), l, s, a);
+        if constexpr (KS <= 24) {
+            if (a.mt1 - a.mt0 <= 2) {             // c <= 32: fewer accumulators, two blocks per wave if short
+                hipLaunchKernelGGL((k_decode_pipe<KS, 2, (KS <= 8 ? 2 : 1)>), grid, dim3(kThreads), l, s, a);
+                return;
+            }
+        }
+        hipLaunchKernelGGL((k_decode_pipe<KS, kMaxRegTiles, 1>), grid, dim3(kThreads), l, s, a);
     }
     else if (path == Path::kFast) hipLaunchKernelGGL((k_decode<KS, true, false, true>), grid, dim3(kThreads), lds, s, a);
     else if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_decode<KS, true, false, false>), grid, dim3(kThreads), lds, s, a);
@@ -884,6 +913,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
         const size_t lds = (size_t)(a.mt1 - a.mt0) * ((ks + 3) / 4) * 256 * sizeof(float) + rows_bytes;
         if (ks <= 4) decode_ks<4>(a, bs, lds, s, N);
         else if (ks <= 8) decode_ks<8>(a, bs, lds, s, N);
+        else if (ks <= 10) decode_ks<10>(a, bs, lds, s, N);
         else if (ks <= 12) decode_ks<12>(a, bs, lds, s, N);
         else if (ks <= 16) decode_ks<16>(a, bs, lds, s, N);
         else if (ks <= 18) decode_ks<18>(a, bs, lds, s, N);
@@ -1072,7 +1102,7 @@ int bucket_layout(const cerar_plan *plan, int nb, const size_t *len, std::vector
     for (int b = 0; b < nb; ++b) {
         if (len[b] == 0) return fail(CERAR_E_INVAL, "bucket %d is empty", b);
         BucketLayout &B = lay[b];
-        B.p = (len[b] + plan->c - 1) / plan->c;
+        B.p = ((len[b] + plan->c - 1) / plan->c + kChunkAlign - 1) / kChunkAlign * kChunkAlign;
         B.stride = (B.p + 63) / 64 * 64;
         B.work_off = work_floats;
         B.ws_off = ws_bytes;

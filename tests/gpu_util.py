@@ -9,6 +9,7 @@ from paper_2609_23898_amd import cerar as C
 from paper_2609_23898_amd import synth
 
 U32 = 2.0 ** -24
+CHUNK_ALIGN = 32          # the library pads chunks to multiples of 32 floats (cerar_chunk_len)
 
 
 def torch_dev():
@@ -62,7 +63,12 @@ def read_slot(plan, d, work, ws, s):
 
 
 def oracle_allreduce(grads, U, R):
-    return OR.allreduce(grads, U, R)
+    """The oracle with the library's chunk length."""
+    return OR.allreduce(grads, U, R, align=CHUNK_ALIGN)
+
+
+def oracle_chunks(g, c):
+    return OR.to_chunks(g, c, align=CHUNK_ALIGN)
 
 
 def rel_l2(a, b):

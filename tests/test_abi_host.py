@@ -14,6 +14,7 @@ import pytest
 
 from conftest import ROOT
 from oracle import plan as P
+from oracle import ring as RG
 from paper_2609_23898_amd import cerar as C
 from paper_2609_23898_amd import synth
 
@@ -205,7 +206,7 @@ def test_chunk_len_and_workspace():
     plan = C.Plan(8, 64, "o_eps", 0.3, seed=2)
     for d in (1, 63, 64, 65, 1000, 1_414_647_808):
         p, stride = plan.chunk_len(d)
-        assert p == -(-d // 64) and stride % 64 == 0 and p <= stride < p + 64
+        assert p == RG.chunk_len(d, 64, 32) and stride % 64 == 0 and p <= stride < p + 64
         assert plan.workspace_bytes(d) == 8 * 8 * stride * 4
 
 

@@ -10,7 +10,8 @@ from oracle import plan as OP
 from oracle import ring as OR
 from paper_2609_23898_amd import cerar as C
 
-from gpu_util import (U32, buffers, gate, host_grads, max_rel_l2, mpc_plan, orthogonal_plan, read_slot,
+from gpu_util import (U32, buffers, gate, host_grads, max_rel_l2, mpc_plan, oracle_allreduce, oracle_chunks,
+                      orthogonal_plan, read_slot,
                       rel_l2, to_device, torch_dev)
 
 pytestmark = pytest.mark.gpu
@@ -39,7 +40,7 @@ def test_encode_with_permutations_is_exact(N, c, d):
     sync()
     p, _ = plan.chunk_len(d)
     for i in range(N):
-        G = OR.to_chunks(g[i], c).astype(np.float32)
+        G = oracle_chunks(g[i], c).astype(np.float32)
         expect = G @ U[i].astype(np.float32)
         got = work[i, :c * p].cpu().numpy().reshape(c, p).T
         np.testing.assert_array_equal(got, expect)
@@ -62,7 +63,7 @@ def test_encode_matches_oracle_within_dot_product_bound(N, c, d, misalign):
     sync()
     p, _ = plan.chunk_len(d)
     for i in range(N):
-        G = OR.to_chunks(g[i], c)
+        G = oracle_chunks(g[i], c)
         exact = OR.encode(G, U[i])
         bound = (c + 4) * U32 * (np.abs(G) @ np.abs(U[i])) + 1e-38
         got = work[i, :c * p].double().cpu().numpy().reshape(c, p).T
@@ -81,7 +82,7 @@ def test_each_round_matches_algorithm1_state(N, c, d):
     g = host_grads(N, d, seed=3)
     grads = to_device(g)
     work, ws, out = buffers(plan, d)
-    Delta = [OR.encode(OR.to_chunks(g[i], c), U[i]) for i in range(N)]
+    Delta = [OR.encode(oracle_chunks(g[i], c), U[i]) for i in range(N)]
     trace = []
     Y, _ = OR.run_protocol(Delta, trace=trace)
     L = c + N - 2
@@ -143,7 +144,7 @@ def test_ring_simulate_parity(name, N, c, d, kind, param):
     C.ring_simulate(plan, d, grads, work, ws, out)
     sync()
     gpu = out.double().cpu().numpy()
-    ref = OR.allreduce(g, U, R)
+    ref = oracle_allreduce(g, U, R)
     S = OR.exact_sum(g)
     parity = max_rel_l2(gpu, ref)
     err_gpu = max(rel_l2(gpu[i], S) for i in range(N))
@@ -186,7 +187,7 @@ def test_edge_shapes(name, N, c, d):
     C.ring_simulate(plan, d, grads, work, ws, out)
     sync()
     gpu = out.double().cpu().numpy()
-    ref = OR.allreduce(g, U, R)
+    ref = oracle_allreduce(g, U, R)
     assert np.all(np.isfinite(gpu))
     assert max_rel_l2(gpu, ref) <= 1e-4, name
     if c == N:
@@ -248,7 +249,7 @@ def test_scalar_layout_matches_vector_layout():
     sync()
     a, b = out.double().cpu().numpy(), out2[:, :d].double().cpu().numpy()
     assert max_rel_l2(b, a) < 1e-6
-    ref = OR.allreduce(g, U, R)
+    ref = oracle_allreduce(g, U, R)
     assert max_rel_l2(b, ref) < 1e-4
 
 
@@ -335,7 +336,7 @@ def test_bucketed_matches_independent_instances():
     sync()
     gpu = out.double().cpu().numpy()
     for off, ln in buckets:
-        ref = OR.allreduce(g[:, off:off + ln], U, R)
+        ref = oracle_allreduce(g[:, off:off + ln], U, R)
         assert max_rel_l2(gpu[:, off:off + ln], ref) < 1e-4
 
 

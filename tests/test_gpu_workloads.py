@@ -21,7 +21,7 @@ from oracle import ring as OR
 from paper_2609_23898_amd import cerar as C
 from paper_2609_23898_amd import synth
 
-from gpu_util import gate, orthogonal_plan, torch_dev
+from gpu_util import CHUNK_ALIGN, gate, orthogonal_plan, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -40,7 +40,7 @@ def host_inputs(wl, pos, c, off=0, length=None):
     sampled positions of the instance [off, off + length) of the flat
     gradient, zero beyond its end (the pad)."""
     length = wl.d if length is None else length
-    p = -(-length // c)
+    p = OR.chunk_len(length, c, CHUNK_ALIGN)
     flat = np.arange(c)[None, :] * p + pos[:, None]
     valid = flat < length
     G = []
@@ -130,7 +130,7 @@ def test_workload2_o_eps():
     work, ws, out = C.allocate(plan, wl.d, dev)
     run_stepwise(plan, wl.d, grads, work, ws, out)
     torch.cuda.synchronize()
-    p = -(-wl.d // wl.c)
+    p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
     parity, err_gpu, err_orc = check_sampled("workload2", wl, U, R, grads, out,
                                              sample_positions(p, 1 << 18, 2), kappa)
     # the O(eps) error is the plan's, not the arithmetic's: eq. (14) bounds Phi
@@ -156,7 +156,7 @@ def test_workload3_gpt2_buckets():
     torch.cuda.synchronize()
     assert not bool(torch.isnan(out).any())            # every bucket wrote all of its d_b outputs
     for bi, (off, ln) in enumerate(wl.buckets):
-        p = -(-ln // wl.c)
+        p = OR.chunk_len(ln, wl.c, CHUNK_ALIGN)
         check_sampled(f"workload3 bucket {bi} (len {ln})", wl, U, R, grads, out,
                       sample_positions(p, 2048, 300 + bi), kappa, off=off, length=ln)
 
@@ -175,7 +175,7 @@ def test_workload4_pythia_headline():
     work, ws, out = C.allocate(plan, wl.d, dev)
     run_stepwise(plan, wl.d, grads, work, ws, out)
     torch.cuda.synchronize()
-    p = -(-wl.d // wl.c)
+    p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
     check_sampled("workload4", wl, U, R, grads, out, sample_positions(p, 65536, 4), kappa)
 
 
@@ -187,7 +187,7 @@ def test_workload5_heavy_tail_n16_c128():
     torch, dev = torch_dev()
     wl = synth.workload(5)
     grads = device_grads(wl, torch, dev)
-    p = -(-wl.d // wl.c)
+    p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
     pos = sample_positions(p, 8192, 5)
     # gated: orthogonal plan at the full shape
     U, R = orthogonal_plan(wl.N, wl.c, seed=55)
@@ -229,7 +229,7 @@ def test_chunks_longer_than_the_fast_path_offsets():
     U, R = orthogonal_plan(wl.N, wl.c, seed=66)
     kappa = OP.max_kappa_M(U)
     plan = C.Plan.explicit(U, R)
-    p = -(-wl.d // wl.c)
+    p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
     assert (12 * p + 64) * 4 >= 1 << 31
     grads = device_grads(wl, torch, dev)
     work, ws, out = C.allocate(plan, wl.d, dev)

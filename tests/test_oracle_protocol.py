@@ -287,6 +287,29 @@ def test_chunking_and_padding():
     np.testing.assert_array_equal(RG.from_chunks(G, 10), g)
 
 
+def test_padded_chunk_length():
+    """A longer chunk length is more zero padding (Sec. II): chunk l is still
+    g[l p:(l+1) p], the tail is zero, and the exact plan still returns the
+    exact sum; p = ceil(d/c) rounded up to the alignment."""
+    g = np.arange(1, 11, dtype=np.float64)       # d = 10, c = 4: p = 3 -> 8 with align 8
+    G = RG.to_chunks(g, 4, align=8)
+    assert G.shape == (8, 4) and RG.chunk_len(10, 4, 8) == 8
+    np.testing.assert_array_equal(G[:, 0], [1, 2, 3, 4, 5, 6, 7, 8])
+    np.testing.assert_array_equal(G[:, 1], [9, 10, 0, 0, 0, 0, 0, 0])
+    np.testing.assert_array_equal(G[:, 2:], 0)
+    np.testing.assert_array_equal(RG.from_chunks(G, 10), g)
+    for d, c, a in [(1, 4, 32), (100, 8, 32), (4096, 4, 32), (1001, 7, 32), (64 * 33 + 1, 64, 32)]:
+        p = RG.chunk_len(d, c, a)
+        assert p % a == 0 and c * p >= d and p - a < -(-d // c) <= p
+    rng = np.random.default_rng(12)
+    N = 4
+    U, R = P.mpc_plan(np.eye(N), np.eye(N))       # exact plan (c = N)
+    grads = rng.standard_normal((N, 301))
+    for a in (1, 32):
+        out = RG.allreduce(grads, U, R, align=a)
+        np.testing.assert_allclose(out, np.broadcast_to(RG.exact_sum(grads), out.shape), atol=1e-12)
+
+
 def test_d_smaller_than_c_and_N2():
     """Degenerate sizes: p = 1 with empty chunks, and the smallest ring."""
     rng = np.random.default_rng(9)
