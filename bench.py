@@ -367,6 +367,26 @@ def main():
     torch.cuda.synchronize()
     ms_ring = (time.perf_counter() - t2) * 1e3 / args.steps
 
+    # workloads with DDP buckets: the bucketed call (one CERAR instance per bucket)
+    bucketed = None
+    if wl.buckets:
+        lens = [b[1] for b in wl.buckets]
+        wf, wsb = plan.bucketed_sizes(lens)
+        bwork = torch.empty((N, wf), dtype=torch.float32, device=dev)
+        bws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        C.ring_simulate_bucketed(plan, wl.buckets, grads, bwork, bws, out)
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        for _ in range(args.steps):
+            C.ring_simulate_bucketed(plan, wl.buckets, grads, bwork, bws, out)
+        torch.cuda.synchronize()
+        ms_b = (time.perf_counter() - t3) * 1e3 / args.steps
+        bbytes = sum(N * C.algorithmic_bytes_per_worker(N, c, plan.chunk_len(ln)[0]) for ln in lens)
+        bucketed = {"buckets": len(lens), "ms_per_step": round(ms_b, 4),
+                    "gbps": round(bbytes / (ms_b * 1e-3) / 1e9, 1)}
+        log(f"bucketed ({len(lens)} buckets): {ms_b:.3f} ms/step, {bucketed['gbps']} GB/s")
+        del bwork, bws
+
     # per-kernel durations from the events
     fam_time, fam_count, fam_bytes = {}, {}, {}
     bw = C.phase_bytes_per_worker(N, c, p)
@@ -441,6 +461,7 @@ def main():
                      "traffic": committed_traffic(dominant)},
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
+        "bucketed": bucketed,
         "copy_gbps": round(copy_gbps, 1),
         "approx_rel_err_max": max(rel_err),
         "plan_info": {k: info[k] for k in ("kappa_M", "kappa_U", "kappa_R", "phi", "phi_closed_form",

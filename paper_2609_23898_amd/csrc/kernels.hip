@@ -16,6 +16,7 @@
 #include <map>
 #include <mutex>
 #include <utility>
+#include <vector>
 
 #include "cerar_internal.hpp"
 
@@ -380,16 +381,15 @@ struct RoundParams {
 
 constexpr int kRoundThreads = 256;
 
+// One workgroup's share of a round for one worker: positions
+// [wg, wg + 1) x 1024 (vector layout) or a grid-stride loop (scalar layout).
 template <int MODE, bool VEC>
-__global__ __launch_bounds__(kRoundThreads) void k_round(RoundParams a) {
-    const int worker = blockIdx.x / a.wg_per_worker;
-    const int wg = blockIdx.x - worker * a.wg_per_worker;
-    const RoundOp op = a.ops[worker];
-    const float *recv = a.sb.ptr(op.recv);
-    const float *sub = MODE >= 1 ? a.sb.ptr(op.sub) : nullptr;   // aliases dst (in place)
-    const float *add = MODE <= 1 ? a.sb.ptr(op.add) : nullptr;
-    float *dst = a.sb.ptr(op.dst);
-    const size_t p = a.sb.p;
+__device__ inline void round_body(const SlotBase &sb, const RoundOp &op, unsigned wg, unsigned wgpw) {
+    const float *recv = sb.ptr(op.recv);
+    const float *sub = MODE >= 1 ? sb.ptr(op.sub) : nullptr;   // aliases dst (in place)
+    const float *add = MODE <= 1 ? sb.ptr(op.add) : nullptr;
+    float *dst = sb.ptr(op.dst);
+    const size_t p = sb.p;
     if (VEC) {
         const size_t i = ((size_t)wg * kRoundThreads + threadIdx.x) * 4;
         if (i < p) {
@@ -399,13 +399,54 @@ __global__ __launch_bounds__(kRoundThreads) void k_round(RoundParams a) {
             nt_store(dst + i, v);
         }
     } else {
-        for (size_t i = (size_t)wg * kRoundThreads + threadIdx.x; i < p; i += (size_t)a.wg_per_worker * kRoundThreads) {
+        for (size_t i = (size_t)wg * kRoundThreads + threadIdx.x; i < p; i += (size_t)wgpw * kRoundThreads) {
             float v = recv[i];
             if (MODE >= 1) v = v - sub[i];
             if (MODE <= 1) v = v + add[i];
             dst[i] = v;
         }
     }
+}
+
+template <int MODE, bool VEC>
+__global__ __launch_bounds__(kRoundThreads) void k_round(RoundParams a) {
+    const int worker = blockIdx.x / a.wg_per_worker;
+    const int wg = blockIdx.x - worker * a.wg_per_worker;
+    round_body<MODE, VEC>(a.sb, a.ops[worker], wg, a.wg_per_worker);
+}
+
+// The same round for a batch of independent instances (buckets) in one
+// launch: instance q owns workgroups [wg0, wg0 + N wgpw) and has its own
+// message length and slot bases; the worker's slot ids are shared.
+constexpr int kMaxBatch = 64;
+
+struct BatchInst {
+    float *work;
+    float *pool;
+    size_t p, pool_stride;
+    unsigned wg0, wgpw;
+};
+
+struct BatchRoundParams {
+    const RoundOp *ops;     // N entries of this round
+    size_t ld_work;
+    int Nc, c, nb;
+    BatchInst b[kMaxBatch];
+};
+
+template <int MODE, bool VEC>
+__global__ __launch_bounds__(kRoundThreads) void k_round_batch(BatchRoundParams a) {
+    int lo = 0, hi = a.nb - 1;                       // last instance with wg0 <= blockIdx.x
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (a.b[mid].wg0 <= blockIdx.x) lo = mid;
+        else hi = mid - 1;
+    }
+    const BatchInst q = a.b[lo];
+    const unsigned local = blockIdx.x - q.wg0;
+    const int worker = (int)(local / q.wgpw);
+    const SlotBase sb{q.work, a.ld_work, q.p, q.pool, q.pool_stride, a.Nc, a.c};
+    round_body<MODE, VEC>(sb, a.ops[worker], local - (unsigned)worker * q.wgpw, q.wgpw);
 }
 
 // ---- K4: decode ----------------------------------------------------------------
@@ -860,6 +901,18 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     return CERAR_OK;
 }
 
+// Workgroups per worker of a round: one 16-byte element per thread, or a
+// grid-stride loop in the scalar layout.
+unsigned round_wgs(size_t p, bool vec) {
+    const size_t w = vec ? (p / 4 + kRoundThreads - 1) / kRoundThreads
+                         : std::min<size_t>((p + kRoundThreads - 1) / kRoundThreads, 1 << 16);
+    return (unsigned)std::max<size_t>(1, w);
+}
+
+int round_mode(const cerar_plan *plan, int k) {
+    return (k <= plan->N - 1) ? 0 : (k + 1 <= plan->c ? 1 : 2);
+}
+
 int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, int k, float *work,
                   size_t ld_work, void *ws, hipStream_t s) {
     const int N = plan->N, c = plan->c, L = plan->L;
@@ -867,14 +920,10 @@ int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &
     RoundParams a;
     a.sb = slot_base(plan, g, work, ld_work, ws);
     a.ops = dc->rounds + (size_t)k * N;
-    if (g.vec) {
-        a.wg_per_worker = (int)((g.p / 4 + kRoundThreads - 1) / kRoundThreads);
-    } else {
-        a.wg_per_worker = (int)std::min<size_t>((g.p + kRoundThreads - 1) / kRoundThreads, 1 << 16);
-    }
-    a.wg_per_worker = std::max(1, a.wg_per_worker);
+    a.wg_per_worker = (int)round_wgs(g.p, g.vec);
     const dim3 grid((unsigned)(N * a.wg_per_worker));
-    const int mode = (k <= N - 1) ? 0 : (k + 1 <= c ? 1 : 2);
+    (void)c;
+    const int mode = round_mode(plan, k);
     if (g.vec) {
         if (mode == 0) hipLaunchKernelGGL((k_round<0, true>), grid, dim3(kRoundThreads), 0, s, a);
         else if (mode == 1) hipLaunchKernelGGL((k_round<1, true>), grid, dim3(kRoundThreads), 0, s, a);
@@ -1147,19 +1196,59 @@ extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets
     st = device_copy(plan, &dc);
     if (st) return st;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    for (int b = 0; b < nbuckets && !st; ++b) {
+    std::vector<Geometry> geo(nbuckets);
+    bool all_vec = true;
+    for (int b = 0; b < nbuckets; ++b) {
         const BucketLayout &B = lay[b];
-        Geometry g;
+        Geometry &g = geo[b];
         g.p = B.p;
         g.pool_stride = B.stride;
-        float *wb = work + B.work_off;
-        void *sb = (char *)ws + B.ws_off;
-        g.vec = (g.p % 4 == 0) && (ld_work % 4 == 0) && aligned16(wb) && aligned16(sb);
-        const float *gb = grads + bucket_off[b];
-        float *ob = out + bucket_off[b];
-        st = enqueue_encode(plan, dc, g, bucket_len[b], gb, ld_grads, wb, ld_work, sb, s);
-        for (int k = 1; k <= plan->L && !st; ++k) st = enqueue_round(plan, dc, g, k, wb, ld_work, sb, s);
-        if (!st) st = enqueue_decode(plan, dc, g, bucket_len[b], wb, ld_work, sb, ob, ld_out, s);
+        g.vec = (g.p % 4 == 0) && (ld_work % 4 == 0) && aligned16(work + B.work_off) &&
+                aligned16((char *)ws + B.ws_off);
+        all_vec = all_vec && g.vec;
     }
+    // every bucket's encode, then each round once for all buckets (up to
+    // kMaxBatch per launch), then every bucket's decode: one stream orders them
+    for (int b = 0; b < nbuckets && !st; ++b)
+        st = enqueue_encode(plan, dc, geo[b], bucket_len[b], grads + bucket_off[b], ld_grads, work + lay[b].work_off,
+                            ld_work, (char *)ws + lay[b].ws_off, s);
+    for (int k = 1; k < plan->L && !st; ++k) {
+        for (int b0 = 0; b0 < nbuckets; b0 += kMaxBatch) {
+            BatchRoundParams a;
+            a.ops = dc->rounds + (size_t)k * N;
+            a.ld_work = ld_work;
+            a.Nc = plan->N * plan->c;
+            a.c = plan->c;
+            a.nb = std::min(kMaxBatch, nbuckets - b0);
+            size_t wgs = 0;
+            for (int q = 0; q < a.nb; ++q) {
+                const BucketLayout &B = lay[b0 + q];
+                BatchInst &I = a.b[q];
+                I.work = work + B.work_off;
+                I.pool = (float *)((char *)ws + B.ws_off);
+                I.p = B.p;
+                I.pool_stride = B.stride;
+                I.wgpw = round_wgs(B.p, all_vec);
+                I.wg0 = (unsigned)wgs;
+                wgs += (size_t)N * I.wgpw;
+            }
+            if (wgs > 0x7fffffffu) return fail(CERAR_E_INVAL, "bucket batch too large for one launch");
+            const dim3 grid((unsigned)wgs);
+            const int mode = round_mode(plan, k);
+            if (all_vec) {
+                if (mode == 0) hipLaunchKernelGGL((k_round_batch<0, true>), grid, dim3(kRoundThreads), 0, s, a);
+                else if (mode == 1) hipLaunchKernelGGL((k_round_batch<1, true>), grid, dim3(kRoundThreads), 0, s, a);
+                else hipLaunchKernelGGL((k_round_batch<2, true>), grid, dim3(kRoundThreads), 0, s, a);
+            } else {
+                if (mode == 0) hipLaunchKernelGGL((k_round_batch<0, false>), grid, dim3(kRoundThreads), 0, s, a);
+                else if (mode == 1) hipLaunchKernelGGL((k_round_batch<1, false>), grid, dim3(kRoundThreads), 0, s, a);
+                else hipLaunchKernelGGL((k_round_batch<2, false>), grid, dim3(kRoundThreads), 0, s, a);
+            }
+            HIP_TRY(hipGetLastError(), "launch bucket round");
+        }
+    }
+    for (int b = 0; b < nbuckets && !st; ++b)
+        st = enqueue_decode(plan, dc, geo[b], bucket_len[b], work + lay[b].work_off, ld_work,
+                            (char *)ws + lay[b].ws_off, out + bucket_off[b], ld_out, s);
     return st;
 }
