@@ -195,9 +195,10 @@ int cerar_ring_simulate(const cerar_plan *plan, size_t d,
  * bucket_off[b] + bucket_len[b]) of every worker's gradient and gets its own
  * p_b (cerar_chunk_len of bucket_len[b]).  work holds, per worker, the buckets' c*p_b
  * slots back to back (stride ld_work >= sum_b c*p_b); ws is
- * cerar_bucketed_workspace_bytes.  The buckets run one after another on
- * `stream`, each as its own encode, round and decode launches (all workers
- * per launch).  bucket_off/bucket_len are host arrays. */
+ * cerar_bucketed_workspace_bytes.  Enqueued on `stream`: every bucket's
+ * encode, then each round as one launch for up to 64 buckets and all
+ * workers, then every bucket's decode.  bucket_off/bucket_len are host
+ * arrays; buckets may not overlap in out. */
 int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len,
                                    int nbuckets, size_t *work_floats, size_t *ws_bytes);
 int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,

@@ -1184,6 +1184,13 @@ extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets
     if (ld_work < work_floats) return fail(CERAR_E_INVAL, "ld_work=%zu < %zu floats of bucket slots", ld_work, work_floats);
     size_t span = 0;
     for (int b = 0; b < nbuckets; ++b) span = std::max(span, bucket_off[b] + bucket_len[b]);
+    {
+        std::vector<std::pair<size_t, size_t>> iv(nbuckets);
+        for (int b = 0; b < nbuckets; ++b) iv[b] = {bucket_off[b], bucket_off[b] + bucket_len[b]};
+        std::sort(iv.begin(), iv.end());
+        for (int b = 1; b < nbuckets; ++b)
+            if (iv[b].first < iv[b - 1].second) return fail(CERAR_E_INVAL, "buckets overlap");
+    }
     if (ld_grads < span || ld_out < span) return fail(CERAR_E_INVAL, "ld_grads and ld_out must cover every bucket");
     const size_t N = plan->N;
     const size_t out_bytes = ((N - 1) * ld_out + span) * sizeof(float);

@@ -200,6 +200,12 @@ def test_device_calls_validate_before_touching_the_device():
     assert lib.cerar_ring_simulate(plan.handle, 0, fake, 1, fake, 1, ws, out, 1, None) == -1
     assert lib.cerar_error_norms(0, 10, fake, 10, out, 10, ws, None) == -1
     assert lib.cerar_copy_f32(None, fake, 10, None) == -1
+    # overlapping buckets
+    offs = (ctypes.c_size_t * 2)(0, 100)
+    lens = (ctypes.c_size_t * 2)(200, 200)
+    assert lib.cerar_ring_simulate_bucketed(plan.handle, 2, offs, lens, fake, 1000, ctypes.c_void_p(0x40000000),
+                                            1 << 20, ws, out, 1000, None) == -1
+    assert b"overlap" in lib.cerar_last_error()
 
 
 def test_chunk_len_and_workspace():
