@@ -24,6 +24,7 @@ namespace cerar {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 // Loads through a pointer the compiler cannot place (one read from LDS, as
 // the decode's row table) would be flat loads, which count against the LDS
 // wait counter too and so serialise the table reads with the data loads.
@@ -36,7 +37,7 @@ __device__ inline float load1_g(const float *ptr) { return *(global_cf *)(ptr); 
 
 constexpr int kThreads = 256;                  // 4 wavefronts of 64
 constexpr int kWaves = kThreads / 64;
-constexpr size_t kLdsBudget = 64 * 1024;       // bytes of LDS a workgroup may use
+constexpr size_t kLdsBudget = 80 * 1024;       // bytes of LDS a workgroup may use (two per 160 KiB CU)
 
 // Address of a p-float slot (see RingTables): the workers' own chunks in
 // `work`, or the per-worker message pool in the workspace.
@@ -138,6 +139,16 @@ __device__ inline uint32_t opaque(uint32_t x) {
 __device__ inline v4f load_off(const float *ubase, uint32_t lane_bytes) {
     return *reinterpret_cast<const v4f *>(reinterpret_cast<const char *>(ubase) + lane_bytes);
 }
+__device__ inline v2f load2_off(const float *ubase, uint32_t lane_bytes) {
+    return *reinterpret_cast<const v2f *>(reinterpret_cast<const char *>(ubase) + lane_bytes);
+}
+__device__ inline v2f nt_load2_g(const float *ptr) {
+    typedef __attribute__((address_space(1))) const v2f global_cv2f;
+    return __builtin_nontemporal_load((global_cv2f *)(ptr));
+}
+__device__ inline void nt_store2_off(float *ubase, uint32_t lane_bytes, v2f v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<v2f *>(reinterpret_cast<char *>(ubase) + lane_bytes));
+}
 __device__ inline void nt_store_off(float *ubase, uint32_t lane_bytes, v4f v) {
     __builtin_nontemporal_store(v, reinterpret_cast<v4f *>(reinterpret_cast<char *>(ubase) + lane_bytes));
 }
@@ -195,6 +206,50 @@ __device__ inline void mtile_mma_lds(v4f (&acc)[4], const v4f (&b)[KS], const fl
                 acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][1], acc[1], 0, 0, 0);
                 acc[2] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][2], acc[2], 0, 0, 0);
                 acc[3] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][3], acc[3], 0, 0, 0);
+            }
+        }
+    }
+}
+
+// Two-component variant: the B operand of K-step ks is a float2 per lane,
+// so one M-tile is two MFMA chains over 32 positions.
+template <int KS>
+__device__ inline void mtile_mma_lds2(v4f (&acc)[2], const v2f (&b)[KS], const float *sfr, int lane) {
+    acc[0] = v4f{0.f, 0.f, 0.f, 0.f};
+    acc[1] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < (KS + 3) / 4; ++q) {
+        const v4f aq = *reinterpret_cast<const v4f *>(sfr + ((size_t)q * 64 + lane) * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int ks = q * 4 + r;
+            if (ks < KS) {
+                acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][0], acc[0], 0, 0, 0);
+                acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][1], acc[1], 0, 0, 0);
+            }
+        }
+    }
+}
+
+// Two M-tiles at once on two-component B operands: four independent MFMA
+// chains, enough to cover the MFMA result latency.
+template <int KS>
+__device__ inline void mtile2_mma_lds2(v4f (&acc)[2][2], const v2f (&b)[KS], const float *sfr0, const float *sfr1,
+                                       int lane) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m) acc[m][0] = acc[m][1] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < (KS + 3) / 4; ++q) {
+        const v4f a0 = *reinterpret_cast<const v4f *>(sfr0 + ((size_t)q * 64 + lane) * 4);
+        const v4f a1 = *reinterpret_cast<const v4f *>(sfr1 + ((size_t)q * 64 + lane) * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int ks = q * 4 + r;
+            if (ks < KS) {
+                acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[r], b[ks][0], acc[0][0], 0, 0, 0);
+                acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[r], b[ks][0], acc[1][0], 0, 0, 0);
+                acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[r], b[ks][1], acc[0][1], 0, 0, 0);
+                acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[r], b[ks][1], acc[1][1], 0, 0, 0);
             }
         }
     }
@@ -363,6 +418,74 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         }
         if (next >= end) break;
         blk = next;
+    }
+}
+
+// Wide encode for c = 16 MTC > 64: at 2c flops per byte the contraction is
+// bound by the fp32 MFMA rate, so one wave per SIMD runs it with two register
+// buffers of B operands: half-block n+1's loads are in flight while half-block
+// n's MTC M-tiles run, and each tile's 16 output rows are stored as soon as it
+// is done.  Half-blocks of 32 positions (a float2 per lane and K-step) keep
+// both buffers in the architectural registers.
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_encode_wide(EncParams a) {
+    static_assert(MTC % 2 == 0, "M-tiles run in pairs");
+    extern __shared__ float sfrag[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int KSx = a.KSe;
+    constexpr int Q = (KS + 3) / 4;
+    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS);
+    __syncthreads();
+    const float *src = a.grads + (size_t)worker * a.ld_g;
+    float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
+    float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
+    const size_t p = a.sb.p;
+    // half-blocks of 32 positions: [2 blk0, 2 blk1)
+    const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
+                 end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
+    size_t hb = first + wave;
+    if (hb >= end) return;
+    v2f b0[KS], b1[KS];
+    auto load = [&](v2f (&b)[KS], size_t h) {
+        const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 2 * (size_t)col) * sizeof(float)));
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = load2_off(src + h * 32 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+    };
+    auto tile = [&](const v2f (&b)[KS], size_t h, int mt) {     // M-tiles mt and mt + 1
+        const size_t e0 = h * 32;
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
+        v4f acc[2][2];
+        mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const v2f v = {acc[m][0][r], acc[m][1][r]};
+                nt_store2_off(dst + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
+                if (mt + m == 0 && krow * 4 + r == 0) nt_store2_off(x1 + e0, (uint32_t)(2 * col * sizeof(float)), v);
+            }
+    };
+    // the next half-block's loads go out after the first M-tile pair, when this
+    // half-block's operands have all arrived: waits stay exact and short
+    load(b0, hb);
+    while (true) {
+        size_t next = hb + kWaves;
+        tile(b0, hb, 0);
+        if (next < end) load(b1, next);
+#pragma unroll
+        for (int mt = 2; mt < MTC; mt += 2) tile(b0, hb, mt);
+        if (next >= end) break;
+        hb = next;
+        next = hb + kWaves;
+        tile(b1, hb, 0);
+        if (next < end) load(b0, next);
+#pragma unroll
+        for (int mt = 2; mt < MTC; mt += 2) tile(b1, hb, mt);
+        if (next >= end) break;
+        hb = next;
     }
 }
 
@@ -601,6 +724,69 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * N
     }
 }
 
+// Wide decode for c = 16 MTC > 64, same scheme as the wide encode; the B
+// rows come through the per-worker table of observation slots.
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_decode_wide(DecParams a) {
+    static_assert(MTC % 2 == 0, "M-tiles run in pairs");
+    extern __shared__ float smem[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int KSx = a.KSd;
+    constexpr int Q = (KS + 3) / 4;
+    float *sfrag = smem;
+    const float **srow = reinterpret_cast<const float **>(smem + (size_t)MTC * Q * 256);
+    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS);
+    for (int t = threadIdx.x; t < 4 * KS; t += kThreads)
+        srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
+    __syncthreads();
+    float *out = a.out + (size_t)worker * a.ld_o;
+    const size_t p = a.sb.p;
+    const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
+                 end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
+    size_t hb = first + wave;
+    if (hb >= end) return;
+    v2f b0[KS], b1[KS];
+    auto load = [&](v2f (&b)[KS], size_t h) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load2_g(srow[ks * 4 + krow] + h * 32 + 2 * col);
+    };
+    auto tile = [&](const v2f (&b)[KS], size_t h, int mt) {     // M-tiles mt and mt + 1
+        const size_t e0 = h * 32;
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
+        v4f acc[2][2];
+        mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const v2f v = {acc[m][0][r], acc[m][1][r]};
+                nt_store2_off(out + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
+            }
+    };
+    // the next half-block's loads go out after the first M-tile pair, when this
+    // half-block's operands have all arrived: waits stay exact and short
+    load(b0, hb);
+    while (true) {
+        size_t next = hb + kWaves;
+        tile(b0, hb, 0);
+        if (next < end) load(b1, next);
+#pragma unroll
+        for (int mt = 2; mt < MTC; mt += 2) tile(b0, hb, mt);
+        if (next >= end) break;
+        hb = next;
+        next = hb + kWaves;
+        tile(b1, hb, 0);
+        if (next < end) load(b0, next);
+#pragma unroll
+        for (int mt = 2; mt < MTC; mt += 2) tile(b1, hb, mt);
+        if (next >= end) break;
+        hb = next;
+    }
+}
+
 // ---- K5: error norms ---------------------------------------------------------
 
 constexpr int kNormWorkers = 8;
@@ -819,6 +1005,7 @@ int mtiles_per_launch(int MT, int KS, size_t extra) {
 struct BlockSplit {
     size_t interior, total;
     Path tail;
+    bool skip_interior = false;   // the interior blocks were launched elsewhere
 };
 
 BlockSplit split_blocks(const cerar_plan *plan, size_t p, size_t d, bool vec) {
@@ -836,7 +1023,7 @@ BlockSplit split_blocks(const cerar_plan *plan, size_t p, size_t d, bool vec) {
 
 template <class Params, class Launch>
 int launch_split(Params a, const BlockSplit &bs, size_t lds, hipStream_t s, int N, Launch launch) {
-    if (bs.interior > 0) {
+    if (bs.interior > 0 && !bs.skip_interior) {
         a.blk0 = 0;
         a.blk1 = bs.interior;
         wg_for(bs.interior, a.wg_per_worker, a.blk_per_wg);
@@ -894,8 +1081,26 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
         if (mtiles_per_launch(plan->MT, ks, 0) < plan->MT)
             return fail(CERAR_E_INVAL, "c=%d exceeds the encode's LDS budget", plan->c);
         const size_t lds = (size_t)plan->MT * ((ks + 3) / 4) * 256 * sizeof(float);
-        if (ks <= 24) encode_ks<24, false>(a, bs, lds, s, N);
-        else encode_ks<32, false>(a, bs, lds, s, N);
+        if (plan->c == 128 && bs.interior > 0) {
+            // c = 128: interior blocks on the wide kernel, the tail on the generic one
+            EncParams w = a;
+            w.blk0 = 0;
+            w.blk1 = bs.interior;
+            wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
+            hipLaunchKernelGGL((k_encode_wide<32, 8>), dim3((unsigned)(N * w.wg_per_worker)), dim3(kThreads),
+                               (size_t)8 * 8 * 256 * sizeof(float), s, w);
+            if (bs.total > bs.interior) {
+                EncParams t = a;
+                t.blk0 = bs.interior;
+                t.blk1 = bs.total;
+                wg_for(bs.total - bs.interior, t.wg_per_worker, t.blk_per_wg);
+                launch_encode_ks<32, false>(t, bs.tail, lds, s, dim3((unsigned)(N * t.wg_per_worker)));
+            }
+        } else if (ks <= 24) {
+            encode_ks<24, false>(a, bs, lds, s, N);
+        } else {
+            encode_ks<32, false>(a, bs, lds, s, N);
+        }
     }
     HIP_TRY(hipGetLastError(), "launch encode");
     return CERAR_OK;
@@ -955,22 +1160,43 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     const BlockSplit bs = split_blocks(plan, g.p, d, vec);
     const int N = plan->N, ks = plan->KSd;
     const size_t rows_bytes = (size_t)4 * kMaxDecodeKS * sizeof(float *) + 16;
+    BlockSplit rest = bs;
+    if (plan->c == 128 && bs.interior > 0 && ks <= 48) {
+        // c = 128: interior blocks on the wide kernel (all 8 M-tiles, one pass
+        // over the observations), the tail below on the generic one
+        DecParams w = a;
+        w.mt0 = 0;
+        w.mt1 = 8;
+        w.blk0 = 0;
+        w.blk1 = bs.interior;
+        wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
+        const dim3 grid((unsigned)(N * w.wg_per_worker));
+        auto lds_for = [](int K4) { return (size_t)8 * (K4 / 4) * 256 * sizeof(float) + (size_t)4 * K4 * sizeof(float *); };
+        if (ks <= 36) hipLaunchKernelGGL((k_decode_wide<36, 8>), grid, dim3(kThreads), lds_for(36), s, w);
+        else if (ks <= 40) hipLaunchKernelGGL((k_decode_wide<40, 8>), grid, dim3(kThreads), lds_for(40), s, w);
+        else if (ks <= 44) hipLaunchKernelGGL((k_decode_wide<44, 8>), grid, dim3(kThreads), lds_for(44), s, w);
+        else hipLaunchKernelGGL((k_decode_wide<48, 8>), grid, dim3(kThreads), lds_for(48), s, w);
+        HIP_TRY(hipGetLastError(), "launch decode");
+        if (bs.total == bs.interior) return CERAR_OK;
+        rest.skip_interior = true;                    // only the tail blocks remain
+    }
     const int step = mtiles_per_launch(plan->MT, ks, rows_bytes);
     for (int mt0 = 0; mt0 < plan->MT; mt0 += step) {
         a.mt0 = mt0;
         a.mt1 = std::min(plan->MT, mt0 + step);
         const size_t lds = (size_t)(a.mt1 - a.mt0) * ((ks + 3) / 4) * 256 * sizeof(float) + rows_bytes;
-        if (ks <= 4) decode_ks<4>(a, bs, lds, s, N);
-        else if (ks <= 8) decode_ks<8>(a, bs, lds, s, N);
-        else if (ks <= 10) decode_ks<10>(a, bs, lds, s, N);
-        else if (ks <= 12) decode_ks<12>(a, bs, lds, s, N);
-        else if (ks <= 16) decode_ks<16>(a, bs, lds, s, N);
-        else if (ks <= 18) decode_ks<18>(a, bs, lds, s, N);
-        else if (ks <= 20) decode_ks<20>(a, bs, lds, s, N);
-        else if (ks <= 24) decode_ks<24>(a, bs, lds, s, N);
-        else if (ks <= 32) decode_ks<32>(a, bs, lds, s, N);
-        else if (ks <= 40) decode_ks<40>(a, bs, lds, s, N);
-        else decode_ks<48>(a, bs, lds, s, N);
+        if (ks <= 4) decode_ks<4>(a, rest, lds, s, N);
+        else if (ks <= 8) decode_ks<8>(a, rest, lds, s, N);
+        else if (ks <= 10) decode_ks<10>(a, rest, lds, s, N);
+        else if (ks <= 12) decode_ks<12>(a, rest, lds, s, N);
+        else if (ks <= 16) decode_ks<16>(a, rest, lds, s, N);
+        else if (ks <= 18) decode_ks<18>(a, rest, lds, s, N);
+        else if (ks <= 20) decode_ks<20>(a, rest, lds, s, N);
+        else if (ks <= 24) decode_ks<24>(a, rest, lds, s, N);
+        else if (ks <= 32) decode_ks<32>(a, rest, lds, s, N);
+        else if (ks <= 36) decode_ks<36>(a, rest, lds, s, N);
+        else if (ks <= 40) decode_ks<40>(a, rest, lds, s, N);
+        else decode_ks<48>(a, rest, lds, s, N);
         HIP_TRY(hipGetLastError(), "launch decode");
     }
     return CERAR_OK;

@@ -49,6 +49,8 @@ CASES = [
     (8, 64, 64 * 700 + 33, 0, 64, 64),
     (8, 64, 64 * 1024, 0, 0, 0),
     (4, 128, 128 * 130, 0, 0, 4),
+    (2, 128, 128 * 640, 0, 0, 0),        # c = 128 interior blocks: the wide MFMA kernels
+    (3, 128, 128 * 640 - 17, 0, 4, 4),   # ... plus a ragged tail on the generic ones
     (16, 32, 32 * 96 + 5, 4, 8, 12),
 ]
 
