@@ -367,6 +367,26 @@ def main():
     torch.cuda.synchronize()
     ms_ring = (time.perf_counter() - t2) * 1e3 / args.steps
 
+    # the single-GPU fused variant (reported beside the ring, never as the value)
+    fused = None
+    if c % 16 == 0 and c <= 64 and (N <= 8 or c <= 32) and d % 4 == 0:
+        C.ring_simulate_fused(plan, d, grads, out)
+        torch.cuda.synchronize()
+        t4 = time.perf_counter()
+        for _ in range(args.steps):
+            C.ring_simulate_fused(plan, d, grads, out)
+        torch.cuda.synchronize()
+        ms_f = (time.perf_counter() - t4) * 1e3 / args.steps
+        step_bytes_ring = N * C.algorithmic_bytes_per_worker(N, c, p)
+        fused = {"ms_per_step": round(ms_f, 4),
+                 "ring_equivalent_gbps": round(step_bytes_ring / (ms_f * 1e-3) / 1e9, 1),
+                 "moved_gbps": round(2 * N * d * 4 / (ms_f * 1e-3) / 1e9, 1),
+                 "tflops": round(N * sum(C.phase_flops_per_worker(N, c, p).values()) / (ms_f * 1e-3) / 1e12, 1),
+                 "note": "one kernel, all workers' states in LDS: only the gradients are read and the "
+                         "outputs written; possible only when every worker shares one device, so it is "
+                         "not the counted ring path"}
+        log(f"fused single-GPU variant: {ms_f:.3f} ms/step")
+
     # workloads with DDP buckets: the bucketed call (one CERAR instance per bucket)
     bucketed = None
     if wl.buckets:
@@ -462,6 +482,7 @@ def main():
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
         "bucketed": bucketed,
+        "fused_variant": fused,
         "copy_gbps": round(copy_gbps, 1),
         "approx_rel_err_max": max(rel_err),
         "plan_info": {k: info[k] for k in ("kappa_M", "kappa_U", "kappa_R", "phi", "phi_closed_form",

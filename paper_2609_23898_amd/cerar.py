@@ -68,6 +68,7 @@ SIGNATURES = {
     "cerar_encode_round": (_I, [_P, _I, _SZ, _P, _SZ, _P, _SZ, _P, _P]),
     "cerar_decode": (_I, [_P, _SZ, _P, _SZ, _P, _P, _SZ, _P]),
     "cerar_ring_simulate": (_I, [_P, _SZ, _P, _SZ, _P, _SZ, _P, _P, _SZ, _P]),
+    "cerar_ring_simulate_fused": (_I, [_P, _SZ, _P, _SZ, _P, _SZ, _P]),
     "cerar_bucketed_workspace_bytes": (_I, [_P, ctypes.POINTER(_SZ), _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]),
     "cerar_ring_simulate_bucketed": (_I, [_P, _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ), _P, _SZ, _P, _SZ,
                                           _P, _P, _SZ, _P]),
@@ -269,6 +270,12 @@ def decode(plan, d, work, ws, out, stream=None):
 def ring_simulate(plan, d, grads, work, ws, out, stream=None):
     _check(lib().cerar_ring_simulate(plan.handle, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
                                      _ptr(ws), _ptr(out), _ld(out), _stream(stream)))
+
+
+def ring_simulate_fused(plan, d, grads, out, stream=None):
+    """The single-GPU fused variant (cerar_ring_simulate_fused)."""
+    _check(lib().cerar_ring_simulate_fused(plan.handle, d, _ptr(grads), _ld(grads), _ptr(out), _ld(out),
+                                           _stream(stream)))
 
 
 def ring_simulate_bucketed(plan, buckets, grads, work, ws, out, stream=None):

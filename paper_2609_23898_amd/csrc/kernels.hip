@@ -787,6 +787,149 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
 }
 
+// ---- single-GPU fused variant (not the counted path) ---------------------------
+// The whole all-reduce for one 64-position block of every worker in one
+// workgroup of N waves (wave w = worker w): the MFMA encode of the block,
+// the L rounds of Algorithm 1 with every worker's encoded chunks and the
+// messages in LDS (one position per lane), and the decode accumulated on
+// MFMA four observations at a time.  Only the gradients are read and only
+// the outputs written, so it moves about a quarter of the counted path's
+// bytes; it exists only where all workers share one device, so it is a
+// reported variant beside the ring, not a replacement for it.
+
+struct FusedParams {
+    const float *grads;
+    size_t ld_g;
+    size_t d;
+    float *out;
+    size_t ld_o;
+    const float *efrag;     // N x MT x KSe x 64
+    const float *dfrag;     // N x MT x KSd x 64
+    size_t p;
+    int N, c, L, KSd;
+    size_t blk0, blk1;
+};
+
+template <int MTC, bool FAST, int MAXT>
+__global__ __launch_bounds__(MAXT) void k_fused(FusedParams a) {
+    constexpr int KSE = 4 * MTC;                 // c = 16 MTC
+    constexpr int C = 16 * MTC;
+    extern __shared__ float sm[];
+    const int N = a.N, L = a.L;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    float *delta = sm;                                   // [N][C][64]
+    float *msg = delta + (size_t)N * C * 64;             // [2][N][64]
+    float *stage = msg + (size_t)2 * N * 64;             // [N][4][64]
+    float *mydelta = delta + (size_t)w * C * 64;
+    float *mystage = stage + (size_t)w * 256;
+    const float *src = a.grads + (size_t)w * a.ld_g;
+    float *out = a.out + (size_t)w * a.ld_o;
+    const float *ef = a.efrag + (size_t)w * MTC * KSE * 64;
+    const float *df = a.dfrag + (size_t)w * MTC * a.KSd * 64;
+    const size_t p = a.p;
+    for (size_t blk = a.blk0 + blockIdx.x; blk < a.blk1; blk += gridDim.x) {
+        const size_t e0 = blk * 64;
+        // encode: delta_w = U_w^T G_w^T on this block (MFMA, A fragments from L2)
+        v4f b[KSE];
+        if (FAST) {
+            const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) b[ks] = load_off(src + e0 + (size_t)(4 * ks) * p, lane_in);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) {
+                const size_t l = (size_t)(4 * ks + krow);
+                b[ks] = load_tile<true>(src + l * p, l * p, e0, col, p, a.d);
+            }
+        }
+#pragma unroll 1
+        for (int mt = 0; mt < MTC; ++mt) {                // one M-tile at a time: its A fragments only
+            v4f acc[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) {
+                const float av = ef[((size_t)mt * KSE + ks) * 64 + lane];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][t], acc[t], 0, 0, 0);
+            }
+            // D fragment: register r of lane (krow, col) is chunk 16 mt + 4 krow + r, positions 4 col + t
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const v4f v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+                *reinterpret_cast<v4f *>(mydelta + (size_t)(16 * mt + 4 * krow + r) * 64 + 4 * col) = v;
+            }
+        }
+        __syncthreads();
+        // rounds: lane = position; x_{w,1} = delta_{w,1}
+        msg[(size_t)w * 64 + lane] = mydelta[lane];
+        v4f dacc[MTC][4];
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) dacc[mt][t] = v4f{0.f, 0.f, 0.f, 0.f};
+        __syncthreads();
+        const int prev = (w + N - 1) % N;
+        int col_y = 0;                                   // next observation column (0..L)
+        // decode coefficients of the next K-step, fetched one K-step (four
+        // rounds) ahead so that their latency hides behind the rounds
+        float dnext[MTC];
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt) dnext[mt] = df[(size_t)mt * a.KSd * 64 + lane];
+        auto observe = [&](float y) {                    // append column col_y of Y_w
+            mystage[(col_y & 3) * 64 + lane] = y;
+            if ((col_y & 3) == 3 || col_y == L) {
+                for (int r = (col_y & 3) + 1; r < 4; ++r) mystage[r * 64 + lane] = 0.f;   // zero rows past L
+                __builtin_amdgcn_wave_barrier();          // LDS runs a wave's accesses in order
+                const v4f yb = *reinterpret_cast<const v4f *>(mystage + krow * 64 + 4 * col);
+                const int ks = col_y >> 2;
+                float dcur[MTC];
+#pragma unroll
+                for (int mt = 0; mt < MTC; ++mt) dcur[mt] = dnext[mt];
+                if (ks + 1 < a.KSd) {
+#pragma unroll
+                    for (int mt = 0; mt < MTC; ++mt) dnext[mt] = df[((size_t)mt * a.KSd + ks + 1) * 64 + lane];
+                }
+#pragma unroll
+                for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+                        dacc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(dcur[mt], yb[t], dacc[mt][t], 0, 0, 0);
+            }
+            ++col_y;
+        };
+        for (int k = 1; k <= L; ++k) {
+            const float recv = msg[(size_t)((k - 1) & 1) * N * 64 + (size_t)prev * 64 + lane];   // x_{w-1,k}
+            observe(recv);                                // B_{w,k} (k < N) or D_{w,k-N+1}
+            if (k < L) {
+                float x;
+                if (k <= N - 1) {
+                    x = recv + mydelta[(size_t)k * 64 + lane];                   // + delta_{w,k+1}
+                } else {
+                    const int j = k - N + 1;
+                    x = recv - mydelta[(size_t)(j - 1) * 64 + lane];             // - delta_{w,j}
+                    if (k + 1 <= C) x += mydelta[(size_t)k * 64 + lane];         // + delta_{w,k+1}
+                }
+                msg[(size_t)(k & 1) * N * 64 + (size_t)w * 64 + lane] = x;
+            }
+            __syncthreads();
+        }
+        observe(mydelta[(size_t)(C - 1) * 64 + lane]);   // column L: D_{w,c} = delta_{w,c}
+        // outputs: register r of lane (krow, col) is output chunk 16 mt + 4 krow + r
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = 16 * mt + 4 * krow + r;
+                const v4f v = {dacc[mt][0][r], dacc[mt][1][r], dacc[mt][2][r], dacc[mt][3][r]};
+                if (FAST) *reinterpret_cast<v4f *>(out + (size_t)m * p + e0 + 4 * col) = v;
+                else store_tile<true>(out + (size_t)m * p, (size_t)m * p, e0, col, p, a.d, v);
+            }
+        __syncthreads();                                  // LDS reused by the next block
+    }
+}
+
 // ---- K5: error norms ---------------------------------------------------------
 
 constexpr int kNormWorkers = 8;
@@ -1322,6 +1465,82 @@ extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float
     if (st) return st;
     std::lock_guard<std::mutex> lk(g_cursor_mu);
     g_cursor[ws] = {plan, plan->L + 1};
+    return CERAR_OK;
+}
+
+namespace {
+// N <= 8 workers: up to 512 threads, so up to 256 registers per lane;
+// 8 < N <= 16 (then c <= 32 by the LDS bound): 1024 threads, 128 registers.
+template <int MTC, int MAXT>
+void launch_fused(const FusedParams &a, const BlockSplit &bs, size_t lds, hipStream_t s) {
+    FusedParams f = a;
+    const unsigned threads = 64u * (unsigned)a.N;
+    if (bs.interior > 0) {
+        f.blk0 = 0;
+        f.blk1 = bs.interior;
+        hipLaunchKernelGGL((k_fused<MTC, true, MAXT>), dim3((unsigned)std::min<size_t>(bs.interior, 2048)),
+                           dim3(threads), lds, s, f);
+    }
+    if (bs.total > bs.interior) {
+        f.blk0 = bs.interior;
+        f.blk1 = bs.total;
+        hipLaunchKernelGGL((k_fused<MTC, false, MAXT>), dim3((unsigned)std::min<size_t>(bs.total - bs.interior, 2048)),
+                           dim3(threads), lds, s, f);
+    }
+}
+}  // namespace
+
+extern "C" int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                         float *out, size_t ld_out, cerar_stream stream) {
+    clear_error();
+    if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
+    if (d == 0 || !grads || !out) return fail(CERAR_E_INVAL, "d > 0 and non-NULL buffers required");
+    const int N = plan->N, c = plan->c;
+    if (c % 16 != 0 || c > 64) return fail(CERAR_E_INVAL, "the fused variant needs c in {16, 32, 48, 64} (c=%d)", c);
+    if (N > 16) return fail(CERAR_E_INVAL, "the fused variant needs N <= 16 (N=%d)", N);
+    size_t p, stride;
+    int st = cerar_chunk_len(plan, d, &p, &stride);
+    if (st) return st;
+    if (ld_grads < d || ld_out < d) return fail(CERAR_E_INVAL, "ld_grads and ld_out must be >= d");
+    if (ld_grads % 4 || ld_out % 4 || !aligned16(grads) || !aligned16(out))
+        return fail(CERAR_E_INVAL, "the fused variant needs 16-byte aligned rows");
+    if (overlap(grads, (((size_t)N - 1) * ld_grads + d) * sizeof(float), out,
+                (((size_t)N - 1) * ld_out + d) * sizeof(float)))
+        return fail(CERAR_E_INVAL, "grads and out overlap");
+    const size_t lds = (size_t)N * 256 * (c + 6);        // chunks, two message buffers, four staged observations
+    if (lds > 160 * 1024) return fail(CERAR_E_INVAL, "N=%d, c=%d needs %zu bytes of LDS", N, c, lds);
+    const DeviceCopy *dc;
+    st = device_copy(plan, &dc);
+    if (st) return st;
+    FusedParams a;
+    a.grads = grads;
+    a.ld_g = ld_grads;
+    a.d = d;
+    a.out = out;
+    a.ld_o = ld_out;
+    a.efrag = dc->enc_frag;
+    a.dfrag = dc->dec_frag;
+    a.p = p;
+    a.N = N;
+    a.c = c;
+    a.L = plan->L;
+    a.KSd = plan->KSd;
+    const BlockSplit bs = split_blocks(plan, p, d, true);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (N <= 8) {
+        switch (c / 16) {
+            case 1: launch_fused<1, 512>(a, bs, lds, s); break;
+            case 2: launch_fused<2, 512>(a, bs, lds, s); break;
+            case 3: launch_fused<3, 512>(a, bs, lds, s); break;
+            default: launch_fused<4, 512>(a, bs, lds, s); break;
+        }
+    } else if (c <= 32) {
+        if (c == 16) launch_fused<1, 1024>(a, bs, lds, s);
+        else launch_fused<2, 1024>(a, bs, lds, s);
+    } else {
+        return fail(CERAR_E_INVAL, "the fused variant needs c <= 32 when N > 8");
+    }
+    HIP_TRY(hipGetLastError(), "launch fused");
     return CERAR_OK;
 }
 

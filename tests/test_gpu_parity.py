@@ -348,3 +348,56 @@ def test_copy_kernel():
         C.copy_f32(dst, src)
         sync()
         assert bool((dst == src).all())
+
+
+# --- single-GPU fused variant (reported, not the counted path) ------------------------
+
+FUSED = [
+    # name, N, c, d
+    ("N8-c64-ragged", 8, 64, 64 * 1536 + 61),
+    ("N4-c16", 4, 16, 16 * 4096),
+    ("N8-c32-tail", 8, 32, 32 * 777 + 5),
+    ("N16-c32", 16, 32, 32 * 640),
+    ("N2-c48", 2, 48, 48 * 300 + 7),
+    ("N8-c64-d1", 8, 64, 1),
+]
+
+
+@pytest.mark.parametrize("name,N,c,d", FUSED, ids=[x[0] for x in FUSED])
+def test_fused_variant_matches_oracle_and_ring(name, N, c, d):
+    torch, dev = torch_dev()
+    U, R = orthogonal_plan(N, c, seed=N * 7 + c) if N < c else OP.mpc_plan(np.eye(N), np.eye(N))
+    U = U * np.random.default_rng(c).uniform(0.5, 2.0, size=(N, 1, c))   # not orthogonal any more
+    R = OP.r_step(U)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=N + c + d)
+    ld = (d + 3) // 4 * 4                            # the fused variant needs 16-byte aligned rows
+    grads = to_device(g, ld=ld)
+    out = torch.full((N, ld), float("nan"), dtype=torch.float32, device=dev)
+    C.ring_simulate_fused(plan, d, grads, out)
+    work, ws, out_ring = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out_ring)
+    sync()
+    assert bool(torch.isnan(out[:, d:]).all())       # nothing written beyond d
+    fused = out[:, :d].double().cpu().numpy()
+    ring = out_ring.double().cpu().numpy()
+    ref = oracle_allreduce(g, U, R)
+    kappa = OP.max_kappa_M(U)
+    parity = max_rel_l2(fused, ref)
+    print(f"fused {name}: kappa_M={kappa:.3g} parity={parity:.3g}")
+    assert np.all(np.isfinite(fused))
+    assert parity <= gate(kappa)
+    assert max_rel_l2(fused, ring) <= 1e-5           # same arithmetic up to rounding order
+
+
+def test_fused_variant_rejects_unsupported_shapes():
+    torch, dev = torch_dev()
+    for N, c in ((4, 128), (16, 64), (4, 20)):
+        U, R = orthogonal_plan(N, c, seed=1)
+        plan = C.Plan.explicit(U, R)
+        d = c * 64
+        g = to_device(host_grads(N, d, seed=1))
+        out = torch.empty((N, d), dtype=torch.float32, device=dev)
+        with pytest.raises(C.CerarError) as ei:
+            C.ring_simulate_fused(plan, d, g, out)
+        assert ei.value.status == -1
