@@ -421,6 +421,71 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     }
 }
 
+// Double-buffered interior encode for c = 16 MTC (up to 64): two register
+// buffers of float4 B operands, so block n+1's loads are in flight during all
+// of block n's MFMA work, and each M-tile's 16 output rows are stored as soon
+// as the tile is done.  Two waves per SIMD in the register budget.
+//
+// The loop header sits after the first M-tile of a block on every path into
+// it: the compiler's wait counts at the header merge the prologue with the
+// back edge, and a header before the first tile made every other block wait
+// for all of the previous block's stores to drain.
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_dbuf(EncParams a) {
+    extern __shared__ float sfrag[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int KSx = a.KSe;
+    constexpr int Q = (KS + 3) / 4;
+    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS);
+    __syncthreads();
+    const float *src = a.grads + (size_t)worker * a.ld_g;
+    float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
+    float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
+    const size_t p = a.sb.p;
+    const size_t first = a.blk0 + (size_t)wg * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
+    size_t blk = first + wave;
+    if (blk >= end) return;
+    v4f b0[KS], b1[KS];
+    auto load = [&](v4f (&b)[KS], size_t bq) {
+        const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = load_off(src + bq * 64 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+    };
+    auto tile = [&](const v4f (&b)[KS], size_t bq, int mt) {
+        const size_t e0 = bq * 64;
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
+        v4f acc[4];
+        mtile_mma_lds<KS>(acc, b, sfrag + (size_t)mt * Q * 256, lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const v4f v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+            nt_store_off(dst + e0 + (size_t)(mt * 16 + r) * p, lane_out, v);
+            if (mt == 0 && krow * 4 + r == 0) nt_store_off(x1 + e0, (uint32_t)(4 * col * sizeof(float)), v);
+        }
+    };
+    load(b0, blk);
+    tile(b0, blk, 0);
+    while (true) {
+        size_t next = blk + kWaves;
+        if (next < end) load(b1, next);
+#pragma unroll
+        for (int mt = 1; mt < MTC; ++mt) tile(b0, blk, mt);
+        if (next >= end) break;
+        blk = next;
+        tile(b1, blk, 0);
+        next = blk + kWaves;
+        if (next < end) load(b0, next);
+#pragma unroll
+        for (int mt = 1; mt < MTC; ++mt) tile(b1, blk, mt);
+        if (next >= end) break;
+        blk = next;
+        tile(b0, blk, 0);
+    }
+}
+
 // Wide encode for c = 16 MTC > 64: at 2c flops per byte the contraction is
 // bound by the fp32 MFMA rate, so one wave per SIMD runs it with two register
 // buffers of B operands: half-block n+1's loads are in flight while half-block
@@ -469,7 +534,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
             }
     };
     // the next half-block's loads go out after the first M-tile pair, when this
-    // half-block's operands have all arrived: waits stay exact and short
+    // half-block's operands have all arrived.  The loop header precedes the
+    // first pair, so every other half-block waits for the previous stores to
+    // drain; a header after the first pair measured slower here, since the
+    // third copy of the pair's code costs scalar-register spills.
     load(b0, hb);
     while (true) {
         size_t next = hb + kWaves;
@@ -724,6 +792,67 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * N
     }
 }
 
+// Double-buffered interior decode for c = 16 MTC (up to 64), same scheme as
+// the double-buffered encode; the B rows come through the per-worker table of
+// observation slots.
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_dbuf(DecParams a) {
+    extern __shared__ float smem[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int KSx = a.KSd;
+    constexpr int Q = (KS + 3) / 4;
+    float *sfrag = smem;
+    const float **srow = reinterpret_cast<const float **>(smem + (size_t)MTC * Q * 256);
+    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS);
+    // rows K..4 KS-1 repeat row K-1, whose coefficients there are zero
+    for (int t = threadIdx.x; t < 4 * KS; t += kThreads)
+        srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
+    __syncthreads();
+    float *out = a.out + (size_t)worker * a.ld_o;
+    const size_t p = a.sb.p;
+    const size_t first = a.blk0 + (size_t)wg * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
+    size_t blk = first + wave;
+    if (blk >= end) return;
+    v4f b0[KS], b1[KS];
+    auto load = [&](v4f (&b)[KS], size_t bq) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load_g(srow[ks * 4 + krow] + bq * 64 + 4 * col);
+    };
+    auto tile = [&](const v4f (&b)[KS], size_t bq, int mt) {
+        const size_t e0 = bq * 64;
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 4 * (size_t)col) * sizeof(float)));
+        v4f acc[4];
+        mtile_mma_lds<KS>(acc, b, sfrag + (size_t)mt * Q * 256, lane);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const v4f v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+            nt_store_off(out + e0 + (size_t)(mt * 16 + r) * p, lane_out, v);   // 16 | c
+        }
+    };
+    // loop header after a first M-tile on every path (see k_encode_dbuf)
+    load(b0, blk);
+    tile(b0, blk, 0);
+    while (true) {
+        size_t next = blk + kWaves;
+        if (next < end) load(b1, next);
+#pragma unroll
+        for (int mt = 1; mt < MTC; ++mt) tile(b0, blk, mt);
+        if (next >= end) break;
+        blk = next;
+        tile(b1, blk, 0);
+        next = blk + kWaves;
+        if (next < end) load(b0, next);
+#pragma unroll
+        for (int mt = 1; mt < MTC; ++mt) tile(b1, blk, mt);
+        if (next >= end) break;
+        blk = next;
+        tile(b0, blk, 0);
+    }
+}
+
 // Wide decode for c = 16 MTC > 64, same scheme as the wide encode; the B
 // rows come through the per-worker table of observation slots.
 template <int KS, int MTC>
@@ -767,7 +896,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
             }
     };
     // the next half-block's loads go out after the first M-tile pair, when this
-    // half-block's operands have all arrived: waits stay exact and short
+    // half-block's operands have all arrived.  The loop header precedes the
+    // first pair, so every other half-block waits for the previous stores to
+    // drain; a header after the first pair measured slower here, since the
+    // third copy of the pair's code costs scalar-register spills.
     load(b0, hb);
     while (true) {
         size_t next = hb + kWaves;
@@ -1096,6 +1228,13 @@ template <int KS, bool AREG>
 void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
     if constexpr (AREG && KS >= 4) {
         if (path == Path::kFast) {
+            if constexpr (KS == 16) {
+                if (a.MT == 4 && a.mt0 == 0 && a.mt1 == 4) {   // c = 64: double-buffered
+                    const size_t l = (size_t)4 * (KS / 4) * 256 * sizeof(float);
+                    hipLaunchKernelGGL((k_encode_dbuf<KS, 4>), grid, dim3(kThreads), l, s, a);
+                    return;
+                }
+            }
             // up to 4 M-tiles: the pipelined kernel, coefficients staged in LDS;
             // NB blocks per wave keep ~16 KB of loads in flight per wave at any c
             constexpr int MTMAX = KS <= 4 ? 1 : (KS <= 8 ? 2 : 4);
@@ -1117,6 +1256,13 @@ void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, 
 
 template <int KS>
 void launch_decode_ks(const DecParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+    if constexpr (KS >= 16 && KS <= 20) {
+        if (path == Path::kFast && a.MT == 4 && a.mt0 == 0 && a.mt1 == 4) {   // c = 64: double-buffered
+            const size_t l = (size_t)4 * ((KS + 3) / 4) * 256 * sizeof(float) + (size_t)4 * KS * sizeof(float *);
+            hipLaunchKernelGGL((k_decode_dbuf<KS, 4>), grid, dim3(kThreads), l, s, a);
+            return;
+        }
+    }
     if (path == Path::kFast && a.mt1 - a.mt0 <= kMaxRegTiles) {
         const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float) +
                          (size_t)4 * KS * sizeof(float *);
