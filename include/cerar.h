@@ -83,6 +83,15 @@ typedef struct {
                              * 1: U-step, projection, R-step, so every R-step fits a projected
                              * U (about half the Phi at N=8, c=32..64).  Both end with a
                              * projection and an R-step, so kappa_2(M_i) <= kappa_max holds. */
+    const int *node_perms;  /* O_EPS, KAPPA, with perturb == NULL: n_node_perms candidate
+                             * permutations of 0..c-1 (host, row-major n x c).  Candidate t is
+                             * H_t = diag(xi[perm_t[0]], ..., xi[perm_t[c-1]]); the plan takes the
+                             * one with the largest gamma = min_l sigma_min(K^(l)(B, H_t)), the
+                             * constant of the Sec. II-C assumption (the first on ties).  A choice
+                             * of H that depends on B, which the same assumption allows.  The
+                             * permutations leave ||H||, D's spectrum and so Phi unchanged, but
+                             * a small gamma makes the windows A_l, and so M_i, ill-conditioned. */
+    int n_node_perms;       /* 0: H as above (perturb, else diag(nodes)); at most 4096 */
 } cerar_plan_desc;
 
 /* Plan diagnostics (host fp64). */
@@ -102,6 +111,9 @@ typedef struct {
     double proj_a0, proj_b0;      /* KAPPA: last projection interval, else NaN */
     int fp64_reliable;            /* 0 when kappa_U * c * 2^-53 > 1e-6: fp64 inverses lose digits */
     uint64_t seed_used;           /* seed that produced B (after retries), 0 if B was given */
+    double gamma;                 /* O_EPS, KAPPA: min_l sigma_min(K^(l)(B, H)) of the (B, H) used
+                                   * (Sec. II-C assumption); NaN otherwise */
+    int h_choice;                 /* index of the chosen node permutation, -1 if none was given */
 } cerar_plan_info;
 
 /* Build a plan on the host in fp64 (Sec. II-B to II-D): B and D (or the
@@ -109,6 +121,7 @@ typedef struct {
  * R_i[l,:] = a_{l-i} (eq. (11)); KAPPA then runs the alternating least squares
  * of Sec. II-D from the O(eps0) plan.  Synchronous; touches no device.
  * Errors: E_INVAL (N < 2, N > 64, c < N, c > 128, param out of range,
+ * node_perms with perturb, with VANDERMONDE or not permutations,
  * out == NULL), E_SINGULAR (a window A_l exactly singular for 8 seeds, or for
  * the given B), E_NOMEM. */
 int cerar_plan_create(int N, int c, cerar_construction kind, double param,

@@ -18,7 +18,12 @@ design notes):
   xi_j = cos((2j-1) pi / (2c)), distinct and inside (-1, 1).
 * O(eps) direction H: the appendix on the experiments says H is diagonal with
   small entries or derived from B; the default here is H = diag(xi) with the
-  same Chebyshev nodes, so ||H||_2 <= 1 and D_eps = I + eps H.
+  same Chebyshev nodes, so ||H||_2 <= 1 and D_eps = I + eps H.  The B-dependent
+  choice taken here assigns the nodes to the columns of B: among given
+  permutations it takes the one whose H = diag(xi[perm]) has the largest gamma,
+  the smallest singular value over the limits K^(l)(B, H) (Sec. II-C
+  assumption), so that the windows A_l(eps) and the maps M_i stay
+  well-conditioned.
 * Constrained design (Sec. II-D): one iteration is a U-step, an R-step, then
   the projection of every U_k's singular values into a common [a0, b0].  The
   interval is centred (geometrically) on the geometric mean s of all current
@@ -181,6 +186,42 @@ def kappa2(X):
 def max_kappa_M(U):
     """max_i kappa_2(M_i(U)), the quantity bounded in eq. (16)."""
     return max(kappa2(coefficient_map(U, i)) for i in range(U.shape[0]))
+
+
+# --- conditioning of the O(eps) windows (Sec. II-C) ---------------------------
+
+def k_matrix(B, H, ell):
+    """K^(l)(B, H): B, BH, ..., BH^(beta-1), then (if s > 0) the rows
+    r in E_l = {l, ..., l+s-1} (mod N) of BH^beta, where c = beta N + s
+    (Sec. II-C; the eps -> 0 limit of the rescaled window rows)."""
+    B = np.asarray(B, dtype=np.float64)
+    H = np.asarray(H, dtype=np.float64)
+    N, c = B.shape
+    beta, s = divmod(c, N)
+    blocks = [B @ np.linalg.matrix_power(H, j) for j in range(beta)]
+    if s:
+        E = [(ell + t) % N for t in range(s)]
+        blocks.append((B @ np.linalg.matrix_power(H, beta))[E])
+    return np.vstack(blocks)
+
+
+def gamma(B, H):
+    """min over l = 0..N-1 of sigma_min(K^(l)(B, H)): the constant of the
+    Sec. II-C assumption."""
+    N = np.asarray(B).shape[0]
+    return min(float(np.linalg.svd(k_matrix(B, H, ell), compute_uv=False)[-1]) for ell in range(N))
+
+
+def select_node_permutation(B, nodes, perms):
+    """Index and gamma of the candidate H_t = diag(nodes[perm_t]) with the
+    largest gamma (the first one on ties)."""
+    nodes = np.asarray(nodes, dtype=np.float64)
+    best, best_t = -1.0, -1
+    for t, perm in enumerate(perms):
+        g = gamma(B, np.diag(nodes[np.asarray(perm)]))
+        if g > best:
+            best, best_t = g, t
+    return best_t, best
 
 
 # --- condition-number-constrained design (Sec. II-D, eq. (16)) --------------

@@ -34,7 +34,8 @@ class PlanDesc(ctypes.Structure):
                 ("base", ctypes.POINTER(ctypes.c_double)),
                 ("perturb", ctypes.POINTER(ctypes.c_double)),
                 ("nodes", ctypes.POINTER(ctypes.c_double)),
-                ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int), ("als_order", ctypes.c_int)]
+                ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int), ("als_order", ctypes.c_int),
+                ("node_perms", ctypes.POINTER(ctypes.c_int)), ("n_node_perms", ctypes.c_int)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -46,7 +47,7 @@ class PlanInfo(ctypes.Structure):
                 ("amplification", ctypes.c_double), ("comm_rate", ctypes.c_double),
                 ("storage_rate", ctypes.c_double), ("proj_a0", ctypes.c_double),
                 ("proj_b0", ctypes.c_double), ("fp64_reliable", ctypes.c_int),
-                ("seed_used", ctypes.c_uint64)]
+                ("seed_used", ctypes.c_uint64), ("gamma", ctypes.c_double), ("h_choice", ctypes.c_int)]
 
 
 _P = ctypes.c_void_p
@@ -132,7 +133,7 @@ class Plan:
     """Encoding/decoding plan (host fp64), see cerar_plan_create_desc."""
 
     def __init__(self, N, c, kind, param=0.0, seed=0, base=None, perturb=None, nodes=None,
-                 eps0=0.0, als_iters=0, als_order=0, _handle=None):
+                 eps0=0.0, als_iters=0, als_order=0, node_perms=None, _handle=None):
         L = lib()
         self._h = _P()
         if _handle is not None:
@@ -149,9 +150,15 @@ class Plan:
                 return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
 
             kind = _KINDS[kind] if isinstance(kind, str) else int(kind)
+            perms, nperm = None, 0
+            if node_perms is not None:
+                pa = np.ascontiguousarray(node_perms, dtype=np.int32)
+                assert pa.ndim == 2 and pa.shape[1] == c, pa.shape
+                keep.append(pa)
+                perms, nperm = pa.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), pa.shape[0]
             desc = PlanDesc(N, c, kind, float(param), int(seed), arr(base, N * c),
                             arr(perturb, c * c), arr(nodes, c), float(eps0), int(als_iters),
-                            int(als_order))
+                            int(als_order), perms, nperm)
             _check(L.cerar_plan_create_desc(ctypes.byref(desc), ctypes.byref(self._h)))
         info = self.info()
         self.N, self.c, self.L = info["N"], info["c"], info["L"]

@@ -13,6 +13,7 @@ namespace cerar {
 // Build limits (validated by cerar_plan_create*).
 constexpr int kMaxN = 64;
 constexpr int kMaxC = 128;
+constexpr int kMaxNodePerms = 4096;    // candidate H permutations per plan
 
 // The MFMA operand tiling of encode/decode: 16 output rows per M-tile, 4
 // reduction rows per K-step, 64 lanes per fragment.

@@ -290,6 +290,34 @@ void fill_info(cerar_plan *p, cerar_construction kind, double param) {
     }
 }
 
+// K^(l)(B, H) of Sec. II-C, c x c row-major: B, BH, ..., BH^(beta-1), then the
+// s rows r in E_l = {l, ..., l+s-1} (mod N) of BH^beta, where c = beta N + s.
+std::vector<double> k_matrix(const std::vector<double> &B, const std::vector<double> &H, int N, int c, int ell) {
+    const int beta = c / N, s = c % N;
+    std::vector<double> K((size_t)c * c), P = B, T((size_t)N * c);      // P = B H^j
+    for (int j = 0; j < beta; ++j) {
+        std::copy(P.begin(), P.end(), K.begin() + (size_t)j * N * c);
+        la::matmul(P.data(), H.data(), T.data(), N, c, c);
+        P.swap(T);
+    }
+    for (int t = 0; t < s; ++t) {
+        const int r = (ell + t) % N;
+        std::copy(P.begin() + (size_t)r * c, P.begin() + (size_t)(r + 1) * c, K.begin() + ((size_t)beta * N + t) * c);
+    }
+    return K;
+}
+
+// gamma = min over l of sigma_min(K^(l)(B, H)); with s = 0 every l gives the same K.
+double gamma_of(const std::vector<double> &B, const std::vector<double> &H, int N, int c) {
+    const int nl = (c % N) ? N : 1;
+    std::vector<double> g(nl);
+    parallel_for(nl, [&](int ell) {
+        std::vector<double> K = k_matrix(B, H, N, c, ell);
+        g[ell] = la::singular_values(K.data(), c, c).back();
+    });
+    return *std::min_element(g.begin(), g.end());
+}
+
 int validate(const cerar_plan_desc *d) {
     if (!d) return fail(CERAR_E_INVAL, "desc is NULL");
     if (d->N < 2 || d->N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [2, %d] (Algorithm 1 needs N >= 2)", d->N, kMaxN);
@@ -311,6 +339,24 @@ int validate(const cerar_plan_desc *d) {
             break;
         default:
             return fail(CERAR_E_INVAL, "unknown construction %d", (int)d->kind);
+    }
+    if (d->n_node_perms < 0 || d->n_node_perms > kMaxNodePerms)
+        return fail(CERAR_E_INVAL, "n_node_perms=%d outside [0, %d]", d->n_node_perms, kMaxNodePerms);
+    if (d->n_node_perms > 0) {
+        if (!d->node_perms) return fail(CERAR_E_INVAL, "node_perms is NULL with n_node_perms=%d", d->n_node_perms);
+        if (d->kind == CERAR_VANDERMONDE)
+            return fail(CERAR_E_INVAL, "node_perms apply to the O(eps) and KAPPA constructions only");
+        if (d->perturb) return fail(CERAR_E_INVAL, "node_perms and perturb are exclusive");
+        std::vector<char> seen(d->c);
+        for (int t = 0; t < d->n_node_perms; ++t) {
+            std::fill(seen.begin(), seen.end(), 0);
+            for (int j = 0; j < d->c; ++j) {
+                const int v = d->node_perms[(size_t)t * d->c + j];
+                if (v < 0 || v >= d->c || seen[v])
+                    return fail(CERAR_E_INVAL, "node_perms row %d is not a permutation of 0..c-1", t);
+                seen[v] = 1;
+            }
+        }
     }
     return CERAR_OK;
 }
@@ -479,6 +525,8 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
     p->L = c + N - 2;
     p->info.phi_initial = kNaN;
     p->info.proj_a0 = p->info.proj_b0 = kNaN;
+    p->info.gamma = kNaN;
+    p->info.h_choice = -1;
     int result = CERAR_OK;
     if (desc->kind == CERAR_VANDERMONDE) {
         // z_j = exp(tau xi_j); b_l = [z_j^l], l < N; D = diag(z_j^N)
@@ -499,9 +547,6 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
                 return fail(CERAR_E_INVAL, "eps ||H||_2 = %g must be < 1 (Sec. II-C)", eps * s.front());
             }
         }
-        p->D.assign((size_t)c * c, 0.0);
-        for (size_t a = 0; a < H.size(); ++a) p->D[a] = eps * H[a];
-        for (int j = 0; j < c; ++j) p->D[(size_t)j * c + j] += 1.0;
         const int tries = desc->base ? 1 : 8;
         for (int t = 0; t < tries; ++t) {
             if (desc->base) {
@@ -511,6 +556,27 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
                 p->B = gaussian_base(desc->seed + (uint64_t)t, N, c);
                 p->info.seed_used = desc->seed + (uint64_t)t;
             }
+            if (desc->n_node_perms > 0) {
+                // the candidate H with the largest gamma for this B (Sec. II-C assumption)
+                double best = -1.0;
+                std::vector<double> Ht((size_t)c * c, 0.0);
+                for (int q = 0; q < desc->n_node_perms; ++q) {
+                    const int *perm = desc->node_perms + (size_t)q * c;
+                    for (int j = 0; j < c; ++j) Ht[(size_t)j * c + j] = nodes[perm[j]];
+                    const double g = gamma_of(p->B, Ht, N, c);
+                    if (g > best) {
+                        best = g;
+                        H = Ht;
+                        p->info.h_choice = q;
+                    }
+                }
+                p->info.gamma = best;
+            } else {
+                p->info.gamma = gamma_of(p->B, H, N, c);
+            }
+            p->D.assign((size_t)c * c, 0.0);
+            for (size_t a = 0; a < H.size(); ++a) p->D[a] = eps * H[a];
+            for (int j = 0; j < c; ++j) p->D[(size_t)j * c + j] += 1.0;
             result = mpc_plan(p);
             if (result != CERAR_E_SINGULAR) break;
         }
@@ -571,6 +637,8 @@ extern "C" int cerar_plan_create_explicit(int N, int c, const double *U, const d
     p->R.assign(R, R + (size_t)N * (p->L + 1) * c);
     p->info.phi_initial = kNaN;
     p->info.proj_a0 = p->info.proj_b0 = kNaN;
+    p->info.gamma = kNaN;
+    p->info.h_choice = -1;
     int result = finish_plan(p, CERAR_EXPLICIT, kNaN, out);
     if (result != CERAR_OK) delete p;
     return result;

@@ -8,8 +8,12 @@ expected squared norm N c times the variance per position, so the mean over
 workers of the squared relative error is Phi / (N * N c).
 
     python -m paper_2609_23898_amd.plan_table [--quick]
+    python -m paper_2609_23898_amd.plan_table --o-eps [--candidates 64]
 
 prints a Markdown table (plans are built by the library on the host, fp64).
+With --o-eps it compares O(eps) plans with H = diag(nodes) against the H
+chosen by gamma among node permutations (Sec. II-C assumption): same Phi,
+different conditioning.
 """
 
 import argparse
@@ -17,6 +21,7 @@ import math
 import time
 
 from . import cerar as C
+from . import synth
 
 
 def rows(grid, iters, orders):
@@ -33,11 +38,37 @@ def rows(grid, iters, orders):
             plan.close()
 
 
+def o_eps_rows(grid, candidates):
+    for N, c, eps in grid:
+        perms = synth.node_permutations(7, candidates, c)
+        base = synth.base_matrix(1000 + N, N, c)
+        t = time.perf_counter()
+        a = C.Plan(N, c, "o_eps", eps, base=base)
+        b = C.Plan(N, c, "o_eps", eps, base=base, node_perms=perms)
+        ia, ib = a.info(), b.info()
+        yield {"N": N, "c": c, "eps": eps, "phi": ib["phi"], "gamma0": ia["gamma"], "gamma": ib["gamma"],
+               "kappa0": ia["kappa_M"], "kappa": ib["kappa_M"], "choice": ib["h_choice"],
+               "seconds": time.perf_counter() - t}
+        a.close()
+        b.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--quick", action="store_true", help="N <= 8 only")
     ap.add_argument("--iters", type=int, default=100)
+    ap.add_argument("--o-eps", action="store_true", help="O(eps) plans: H = diag(nodes) vs the largest-gamma H")
+    ap.add_argument("--candidates", type=int, default=64)
     args = ap.parse_args()
+    if args.o_eps:
+        grid = [(N, c, eps) for N in ((4, 8) if args.quick else (4, 8, 16)) for c in (N * 2, N * 2 + N // 2, N * 4)
+                for eps in (1e-2, 1e-1) if c <= 128]
+        print("| N | c | eps | Phi | gamma, H = diag(nodes) | kappa_2(M_i) | gamma, chosen H | kappa_2(M_i) | candidate | s |")
+        print("|---|---|---|---|---|---|---|---|---|---|")
+        for r in o_eps_rows(grid, args.candidates):
+            print(f"| {r['N']} | {r['c']} | {r['eps']:.0e} | {r['phi']:.4g} | {r['gamma0']:.3g} | {r['kappa0']:.3g} | "
+                  f"{r['gamma']:.3g} | {r['kappa']:.3g} | {r['choice']} | {r['seconds']:.1f} |", flush=True)
+        return
     Ns = (4, 8) if args.quick else (4, 8, 16)
     grid = []
     for N in Ns:

@@ -1,5 +1,6 @@
-"""Seeded synthetic inputs: gradients shaped like the paper's workloads, and
-the random base matrix of the O(eps) plan.
+"""Seeded synthetic inputs: gradients shaped like the paper's workloads, the
+random base matrix of the O(eps) plan and candidate node permutations for
+its perturbation.
 
 This module is the only code that both the HIP library's callers and the
 oracle's callers use.  It contains none of the method's arithmetic.  It only
@@ -35,6 +36,7 @@ _MUL2 = 0x94D049BB133111EB
 _HASHES_PER_ENTRY = 8            # 6 for the normal, 1 for the outlier mask, 1 spare
 _SCALE_STREAM = 0x5CA1E
 _BASE_STREAM = 0xBA5E
+_PERM_STREAM = 0x9E7
 
 DDP_BUCKET_FLOATS = 25 * 1024 * 1024 // 4    # 25 MiB of fp32, DDP's default cap
 
@@ -273,6 +275,19 @@ def base_matrix(seed, N, c):
     """N x c base matrix B with i.i.d. approximately N(0,1) entries (the paper's
     choice of B for the O(eps) plan, appendix on the experiments), float64."""
     return normal_np(stream_key(seed, _BASE_STREAM), np.arange(N * c)).reshape(N, c)
+
+
+def node_permutations(seed, count, c):
+    """count x c int32 candidate permutations of the c plan nodes: row 0 is
+    the identity, row t > 0 orders 0..c-1 by 64-bit hash keys of counters
+    t*c .. t*c+c-1 (ties, which have probability ~c^2 2^-64, keep index order)."""
+    perms = np.empty((count, c), dtype=np.int32)
+    perms[0] = np.arange(c)
+    key = stream_key(seed, _PERM_STREAM)
+    for t in range(1, count):
+        h = _hash_np(key, np.arange(t * c, (t + 1) * c, dtype=np.int64), 0)
+        perms[t] = np.argsort(h, kind="stable")
+    return perms
 
 
 def workload(cfg):

@@ -87,6 +87,61 @@ def test_mpc_plans_match_oracle(N, c, kind, param):
         assert info["phi_closed_form"] == pytest.approx(P.phi_vandermonde_closed_form(N, param, P.chebyshev_nodes(c)), rel=1e-12)
 
 
+@pytest.mark.parametrize("N,c,eps", [(8, 16, 0.1), (4, 10, 0.1), (4, 8, 0.05), (3, 7, 0.2)])
+def test_node_permutation_choice_matches_oracle(N, c, eps):
+    """With candidate node permutations the library takes the H of the
+    largest gamma (Sec. II-C assumption) and builds the same plan as the
+    oracle from that H; without them it reports gamma of diag(nodes)."""
+    B = synth.base_matrix(5, N, c)
+    perms = synth.node_permutations(9, 24, c)
+    xi = P.chebyshev_nodes(c)
+    plain = C.Plan(N, c, "o_eps", eps, base=B).info()
+    assert plain["h_choice"] == -1
+    assert plain["gamma"] == pytest.approx(P.gamma(B, np.diag(xi)), rel=1e-9)
+    plan = C.Plan(N, c, "o_eps", eps, base=B, node_perms=perms)
+    info = plan.info()
+    t, g = P.select_node_permutation(B, xi, perms)
+    assert info["h_choice"] == t and info["gamma"] == pytest.approx(g, rel=1e-9)
+    assert info["gamma"] >= plain["gamma"] * (1 - 1e-12)          # the identity is candidate 0
+    D = P.o_eps_perturbation(np.diag(xi[perms[t]]), eps)
+    Uo, Ro = P.mpc_plan(B, D)
+    U, R = plan.matrices()
+    np.testing.assert_allclose(U, Uo, rtol=0, atol=1e-13 * max(1.0, info["kappa_U"]) * np.abs(Uo).max())
+    np.testing.assert_allclose(R, Ro, rtol=0, atol=1e-13 * np.abs(Ro).max())
+    assert info["phi"] == pytest.approx(plain["phi"], rel=1e-8)      # same node set, same Phi
+    assert info["kappa_M"] == pytest.approx(P.max_kappa_M(Uo), rel=1e-6)
+
+
+def test_node_permutations_start_the_kappa_design():
+    """The KAPPA design starts from the O(eps0) plan of the chosen H."""
+    N, c = 4, 9
+    B = synth.base_matrix(13, N, c)
+    perms = synth.node_permutations(2, 16, c)
+    xi = P.chebyshev_nodes(c)
+    t, _ = P.select_node_permutation(B, xi, perms)
+    plan = C.Plan(N, c, "kappa", 1e3, base=B, eps0=0.3, als_iters=6, als_order=1, node_perms=perms)
+    assert plan.info()["h_choice"] == t
+    Uo, Ro = P.kappa_design(B, np.diag(xi[perms[t]]), 0.3, 1e3, 6, order="projected")
+    U, R = plan.matrices()
+    np.testing.assert_allclose(U, Uo, rtol=0, atol=1e-7 * np.abs(Uo).max())
+    np.testing.assert_allclose(R, Ro, rtol=0, atol=1e-7 * np.abs(Ro).max())
+
+
+def test_invalid_node_permutations():
+    B = synth.base_matrix(1, 4, 6)
+    good = synth.node_permutations(1, 3, 6)
+    bad = good.copy()
+    bad[1, 0] = bad[1, 1]                                          # a repeated index
+    cases = [dict(kind="o_eps", param=0.1, node_perms=bad),
+             dict(kind="o_eps", param=0.1, node_perms=good, perturb=np.eye(6)),
+             dict(kind="vandermonde", param=0.3, node_perms=good),
+             dict(kind="o_eps", param=0.1, node_perms=np.zeros((4097, 6), dtype=np.int32) + np.arange(6))]
+    for kw in cases:
+        with pytest.raises(C.CerarError) as ei:
+            C.Plan(4, 6, base=None if kw["kind"] == "vandermonde" else B, **kw)
+        assert ei.value.status == -1
+
+
 def test_exact_plan_phi_zero():
     plan = C.Plan(4, 4, "o_eps", 0.0, base=synth.base_matrix(3, 4, 4))
     assert plan.info()["phi"] < 1e-20

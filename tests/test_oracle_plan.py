@@ -293,3 +293,89 @@ def test_vandermonde_base_rows_are_node_powers():
         np.testing.assert_allclose(B[ell] / B[ell - 1], np.exp(tau * xi), rtol=1e-14)
     np.testing.assert_allclose(np.diag(D), np.exp(N * tau * xi), rtol=1e-14)
     assert len(set(np.round(xi, 12))) == c and np.all(np.abs(xi) < 1)
+
+
+# --- K^(l)(B, H) and gamma (Sec. II-C) -----------------------------------------
+
+def _forward_differences(n):
+    """F_n: row k takes the k-th forward difference of a sequence's first n terms."""
+    from math import comb
+    F = np.zeros((n, n))
+    for k in range(n):
+        for i in range(k + 1):
+            F[k, i] = (-1) ** (k - i) * comb(k, i)
+    return F
+
+
+@pytest.mark.parametrize("N,c", [(2, 5), (3, 7), (4, 8), (4, 10), (5, 5)])
+def test_k_matrix_is_the_limit_of_the_differenced_window(N, c):
+    """Group the rows a_l .. a_{l+c-1} of A_l(eps) by remainder mod N, take
+    forward differences within each class and divide the k-th by eps^k: the
+    rows are exactly b_r D^m H^k (D = I + eps H commutes with H), and at
+    eps = 0 they are K^(l)(B, H) up to row order (Sec. II-C, eq. (15)).  Also
+    pins the class counts n_r(l) and first offsets m_r(l) stated there."""
+    rng = np.random.default_rng(400 + N * c)
+    B = rand_base(rng, N, c)
+    H = np.diag(P.chebyshev_nodes(c)) + 0.2 * rng.standard_normal((c, c))   # D and H commute for any H
+    beta, s = divmod(c, N)
+    eps = 0.2
+    D = P.o_eps_perturbation(H, eps)
+    for ell in range(N):
+        A = P.mpc_window(B, D, ell)
+        E = {(ell + t) % N for t in range(s)}
+        limit_rows = []
+        for r in range(N):
+            idx = [j for j in range(ell, ell + c) if j % N == r]
+            assert len(idx) == (beta + 1 if r in E else beta)
+            m = 0 if r >= ell else 1
+            assert idx[0] == r + N * m
+            diffs = _forward_differences(len(idx)) @ A[[j - ell for j in idx]]
+            for k in range(len(idx)):
+                expect = eps ** k * B[r] @ np.linalg.matrix_power(D, m) @ np.linalg.matrix_power(H, k)
+                np.testing.assert_allclose(diffs[k], expect, rtol=0, atol=1e-11)
+                limit_rows.append(B[r] @ np.linalg.matrix_power(H, k))
+        Kref = np.vstack(limit_rows)
+        K = P.k_matrix(B, H, ell)
+        assert K.shape == (c, c)
+        np.testing.assert_allclose(K.T @ K, Kref.T @ Kref, rtol=1e-12, atol=1e-12)
+
+
+def test_gamma_special_cases():
+    """gamma is homogeneous of degree 1 in B, does not depend on l when N | c,
+    and vanishes when H = I makes the blocks of K repeat (beta >= 2)."""
+    rng = np.random.default_rng(7)
+    N, c = 4, 10
+    B = rand_base(rng, N, c)
+    H = np.diag(P.chebyshev_nodes(c))
+    assert P.gamma(3.0 * B, H) == pytest.approx(3.0 * P.gamma(B, H), rel=1e-12)
+    assert P.gamma(B, H) > 0
+    assert P.gamma(B, np.eye(c)) < 1e-12
+    B8 = rand_base(rng, 4, 8)
+    H8 = np.diag(P.chebyshev_nodes(8))
+    K0 = P.k_matrix(B8, H8, 0)
+    for ell in range(1, 4):
+        np.testing.assert_array_equal(P.k_matrix(B8, H8, ell), K0)
+
+
+def test_node_permutation_keeps_phi_and_tracks_conditioning():
+    """Permuting the nodes of a diagonal H leaves D's spectrum and so the
+    Prop. 2 value of Phi unchanged, while gamma and the conditioning of the
+    maps M_i change: the candidate with the largest gamma is better
+    conditioned than the one with the smallest."""
+    rng = np.random.default_rng(11)
+    N, c, eps = 8, 16, 0.1
+    B = rand_base(rng, N, c)
+    nodes = P.chebyshev_nodes(c)
+    perms = [np.arange(c)] + [rng.permutation(c) for _ in range(15)]
+    gammas = [P.gamma(B, np.diag(nodes[p])) for p in perms]
+    t, g = P.select_node_permutation(B, nodes, perms)
+    assert g == max(gammas) and t == int(np.argmax(gammas))
+    phis, kms = [], []
+    for p in (perms[t], perms[int(np.argmin(gammas))]):
+        D = P.o_eps_perturbation(np.diag(nodes[p]), eps)
+        U, R = P.mpc_plan(B, D)
+        phis.append(P.phi(U, R))
+        kms.append(P.max_kappa_M(U))
+    assert phis[0] == pytest.approx(phis[1], rel=1e-9)
+    assert phis[0] == pytest.approx(P.phi_mpc_closed_form(N, P.o_eps_perturbation(np.diag(nodes), eps)), rel=1e-9)
+    assert kms[0] < kms[1] / 3

@@ -128,3 +128,17 @@ def test_base_matrix_is_seeded():
     np.testing.assert_array_equal(a, synth.base_matrix(7, 8, 64))
     assert not np.array_equal(a, synth.base_matrix(8, 8, 64))
     assert math.isclose(float(np.std(synth.base_matrix(1, 64, 64))), 1.0, rel_tol=0.05)
+
+
+def test_node_permutations():
+    """Row 0 is the identity, every row is a permutation of 0..c-1, rows are
+    distinct, and the table is a pure function of (seed, count, c)."""
+    P = synth.node_permutations(3, 40, 16)
+    assert P.shape == (40, 16) and P.dtype == np.int32
+    np.testing.assert_array_equal(P[0], np.arange(16))
+    for row in P:
+        np.testing.assert_array_equal(np.sort(row), np.arange(16))
+    assert len({tuple(r) for r in P}) == 40
+    np.testing.assert_array_equal(P, synth.node_permutations(3, 40, 16))
+    np.testing.assert_array_equal(P[:7], synth.node_permutations(3, 7, 16))
+    assert not np.array_equal(P, synth.node_permutations(4, 40, 16))
