@@ -211,26 +211,6 @@ __device__ inline void mtile_mma_lds(v4f (&acc)[4], const v4f (&b)[KS], const fl
     }
 }
 
-// Two-component variant: the B operand of K-step ks is a float2 per lane,
-// so one M-tile is two MFMA chains over 32 positions.
-template <int KS>
-__device__ inline void mtile_mma_lds2(v4f (&acc)[2], const v2f (&b)[KS], const float *sfr, int lane) {
-    acc[0] = v4f{0.f, 0.f, 0.f, 0.f};
-    acc[1] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int q = 0; q < (KS + 3) / 4; ++q) {
-        const v4f aq = *reinterpret_cast<const v4f *>(sfr + ((size_t)q * 64 + lane) * 4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int ks = q * 4 + r;
-            if (ks < KS) {
-                acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][0], acc[0], 0, 0, 0);
-                acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(aq[r], b[ks][1], acc[1], 0, 0, 0);
-            }
-        }
-    }
-}
-
 // Two M-tiles at once on two-component B operands: four independent MFMA
 // chains, enough to cover the MFMA result latency.
 template <int KS>
@@ -960,10 +940,9 @@ __global__ __launch_bounds__(MAXT) void k_fused(FusedParams a) {
     const float *ef = a.efrag + (size_t)w * MTC * KSE * 64;
     const float *df = a.dfrag + (size_t)w * MTC * a.KSd * 64;
     const size_t p = a.p;
-    for (size_t blk = a.blk0 + blockIdx.x; blk < a.blk1; blk += gridDim.x) {
-        const size_t e0 = blk * 64;
-        // encode: delta_w = U_w^T G_w^T on this block (MFMA, A fragments from L2)
-        v4f b[KSE];
+    v4f b[KSE];                                          // this block's gradient rows
+    auto load_block = [&](size_t bq) {
+        const size_t e0 = bq * 64;
         if (FAST) {
             const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
 #pragma unroll
@@ -975,6 +954,11 @@ __global__ __launch_bounds__(MAXT) void k_fused(FusedParams a) {
                 b[ks] = load_tile<true>(src + l * p, l * p, e0, col, p, a.d);
             }
         }
+    };
+    if (a.blk0 + blockIdx.x < a.blk1) load_block(a.blk0 + blockIdx.x);
+    for (size_t blk = a.blk0 + blockIdx.x; blk < a.blk1; blk += gridDim.x) {
+        const size_t e0 = blk * 64;
+        // encode: delta_w = U_w^T G_w^T on this block (MFMA, A fragments from L2)
 #pragma unroll 1
         for (int mt = 0; mt < MTC; ++mt) {                // one M-tile at a time: its A fragments only
             v4f acc[4];
@@ -1009,6 +993,8 @@ __global__ __launch_bounds__(MAXT) void k_fused(FusedParams a) {
         float dnext[MTC];
 #pragma unroll
         for (int mt = 0; mt < MTC; ++mt) dnext[mt] = df[(size_t)mt * a.KSd * 64 + lane];
+        // the next block's gradient rows load during this block's rounds and decode
+        if (blk + gridDim.x < a.blk1) load_block(blk + gridDim.x);
         auto observe = [&](float y) {                    // append column col_y of Y_w
             mystage[(col_y & 3) * 64 + lane] = y;
             if ((col_y & 3) == 3 || col_y == L) {
