@@ -382,7 +382,7 @@ def main():
                  "ring_equivalent_gbps": round(step_bytes_ring / (ms_f * 1e-3) / 1e9, 1),
                  "moved_gbps": round(2 * N * d * 4 / (ms_f * 1e-3) / 1e9, 1),
                  "tflops": round(N * sum(C.phase_flops_per_worker(N, c, p).values()) / (ms_f * 1e-3) / 1e12, 1),
-                 "note": "one kernel, all workers' states in LDS: only the gradients are read and the "
+                 "note": "one kernel, all workers' messages on chip: only the gradients are read and the "
                          "outputs written; possible only when every worker shares one device, so it is "
                          "not the counted ring path"}
         log(f"fused single-GPU variant: {ms_f:.3f} ms/step")
@@ -478,7 +478,8 @@ def main():
                    "bytes_per_step": step_bytes, "encode": "out of place (grads kept for every step)"},
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
-                     "traffic": committed_traffic(dominant)},
+                     # the committed counter summary covers the headline workload only
+                     "traffic": committed_traffic(dominant) if args.config == 4 else None},
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
         "bucketed": bucketed,

@@ -206,13 +206,16 @@ int cerar_ring_simulate(const cerar_plan *plan, size_t d,
 /* Single-GPU fused variant (not a ring implementation): the same result as
  * cerar_ring_simulate up to rounding order, computed by one kernel that runs
  * the encode, the L rounds of Algorithm 1 and the decode for all N workers
- * on one 64-position block at a time, with the encoded chunks and messages
- * in LDS; only grads are read and only out is written (no work or ws).  It
- * shows what sharing one device allows and is reported beside the ring, never
- * in its place: a real ring must move every message through memory.
- * Needs c in {16, 32, 48, 64}, N <= 8 (or N <= 16 with c <= 32), N (c + 6)
- * 256 bytes of LDS <= 160 KiB, and 16-byte aligned rows (ld % 4 == 0).
- * Errors: E_INVAL. */
+ * on one 64-position block at a time, with the encoded chunks, messages and
+ * observations on chip (LDS and registers); only grads are read and only out
+ * is written (no work or ws).  It shows what sharing one device allows and is
+ * reported beside the ring, never in its place: a real ring must move every
+ * message through memory.  For N in {2, 4, 8} the messages pass between
+ * lanes with no workgroup barrier per round.
+ * Needs c in {16, 32, 48, 64}, N <= 8 (or N <= 16 with c <= 32), at most
+ * 160 KiB of LDS (N (c + 6) 256 bytes; for N in {2, 4, 8} also
+ * N max(64 c, 256 ceil((c + N - 1) / 4)) 4 bytes), and 16-byte aligned rows
+ * (ld % 4 == 0).  Errors: E_INVAL. */
 int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
                               float *out, size_t ld_out, cerar_stream stream);
 

@@ -1048,6 +1048,137 @@ __global__ __launch_bounds__(MAXT) void k_fused(FusedParams a) {
     }
 }
 
+
+// Fused variant for N in {2, 4, 8}: the rounds run without workgroup
+// barriers.  One workgroup of N waves takes one 64-position block:
+//  1. encode: wave w = worker w, MFMA, delta_w into LDS as [C][64];
+//  2. rounds: lane (rw, rq) of wave v owns worker rw = lane / (64/N) at block
+//     position v (64/N) + rq; it holds that position's c encoded chunks in
+//     registers, receives x_{rw-1,k} from the lane of worker rw-1 at the same
+//     position by a lane permute, and appends each observation to Y_rw in LDS
+//     (the LDS of step 1, free once the chunks are in registers);
+//  3. decode: wave w = worker w, MFMA over Y_w's K observation rows.
+// Three workgroup barriers per block, against one per round in k_fused.
+template <int MTC, int NW, bool FAST>
+__global__ __launch_bounds__(64 * NW) void k_fused_lanes(FusedParams a) {
+    constexpr int C = 16 * MTC, KSE = 4 * MTC, L = C + NW - 2, K = L + 1;
+    constexpr int KSD = (K + 3) / 4;
+    constexpr int PW = 64 / NW;                      // block positions per wave in the rounds
+    constexpr int DS = C * 64 + 8;                   // LDS floats per worker: delta [C][64] (+8: banks)
+    constexpr int YS = 4 * KSD * 64 + 8;             // LDS floats per worker: Y [4 KSD][64]
+    extern __shared__ float sm[];
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int rw = lane / PW, rpos = w * PW + lane % PW;          // this lane's worker and position in the rounds
+    const int prev_addr = ((((rw + NW - 1) % NW) * PW + lane % PW)) * 4;   // lane of worker rw-1, same position
+    const float *src = a.grads + (size_t)w * a.ld_g;
+    float *out = a.out + (size_t)w * a.ld_o;
+    const float *ef = a.efrag + (size_t)w * MTC * KSE * 64;
+    const float *df = a.dfrag + (size_t)w * MTC * KSD * 64;
+    const size_t p = a.p;
+    v4f b[KSE];                                          // this block's gradient rows
+    auto load_block = [&](size_t bq) {
+        const size_t e0 = bq * 64;
+        if (FAST) {
+            const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 4 * (size_t)col) * sizeof(float)));
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) b[ks] = load_off(src + e0 + (size_t)(4 * ks) * p, lane_in);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) {
+                const size_t l = (size_t)(4 * ks + krow);
+                b[ks] = load_tile<true>(src + l * p, l * p, e0, col, p, a.d);
+            }
+        }
+    };
+    if (a.blk0 + blockIdx.x < a.blk1) load_block(a.blk0 + blockIdx.x);
+    for (size_t blk = a.blk0 + blockIdx.x; blk < a.blk1; blk += gridDim.x) {
+        const size_t e0 = blk * 64;
+        // 1. encode: delta_w = U_w^T G_w^T on this block
+        float *mydelta = sm + (size_t)w * DS;
+#pragma unroll 1
+        for (int mt = 0; mt < MTC; ++mt) {
+            v4f acc[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) {
+                const float av = ef[((size_t)mt * KSE + ks) * 64 + lane];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][t], acc[t], 0, 0, 0);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const v4f v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+                *reinterpret_cast<v4f *>(mydelta + (size_t)(16 * mt + 4 * krow + r) * 64 + 4 * col) = v;
+            }
+        }
+        __syncthreads();
+        // 2. rounds, one (worker, position) per lane
+        float dl[C];
+#pragma unroll
+        for (int j = 0; j < C; ++j) dl[j] = sm[(size_t)rw * DS + (size_t)j * 64 + rpos];
+        // the next block's gradient rows load during the rounds and the decode
+        if (blk + gridDim.x < a.blk1) load_block(blk + gridDim.x);
+        __syncthreads();                                 // every lane has its chunks: LDS now holds Y
+        float *Y = sm + (size_t)rw * YS + rpos;          // column k of Y_rw at Y[64 k]
+        float x = dl[0];                                 // x_{rw,1} = delta_{rw,1}
+#pragma unroll
+        for (int k = 1; k <= L; ++k) {
+            const float recv = __int_as_float(__builtin_amdgcn_ds_bpermute(prev_addr, __float_as_int(x)));
+            Y[(size_t)(k - 1) * 64] = recv;              // x_{rw-1,k}: B_{rw,k} (k < N) or D_{rw,k-N+1}
+            if (k < L) {
+                if (k <= NW - 1) {
+                    x = recv + dl[k];                    // + delta_{rw,k+1}
+                } else {
+                    x = recv - dl[k - NW];               // - delta_{rw,k-N+1}
+                    if (k + 1 <= C) x += dl[k];          // + delta_{rw,k+1}
+                }
+            }
+        }
+        Y[(size_t)L * 64] = dl[C - 1];                   // column L: D_{rw,c} = delta_{rw,c}
+#pragma unroll
+        for (int k = K; k < 4 * KSD; ++k) Y[(size_t)k * 64] = 0.f;   // rows past L meet zero coefficients
+        __syncthreads();
+        // 3. decode: ghat_w = Y_w R_w, output chunk 16 mt + 4 krow + r in register r
+        const float *Yw = sm + (size_t)w * YS;
+        v4f dacc[MTC][4];
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) dacc[mt][t] = v4f{0.f, 0.f, 0.f, 0.f};
+        float dnext[MTC];
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt) dnext[mt] = df[(size_t)mt * KSD * 64 + lane];
+#pragma unroll 2
+        for (int ks = 0; ks < KSD; ++ks) {
+            float dcur[MTC];
+#pragma unroll
+            for (int mt = 0; mt < MTC; ++mt) dcur[mt] = dnext[mt];
+            if (ks + 1 < KSD) {
+#pragma unroll
+                for (int mt = 0; mt < MTC; ++mt) dnext[mt] = df[((size_t)mt * KSD + ks + 1) * 64 + lane];
+            }
+            const v4f yb = *reinterpret_cast<const v4f *>(Yw + (size_t)(4 * ks + krow) * 64 + 4 * col);
+#pragma unroll
+            for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    dacc[mt][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(dcur[mt], yb[t], dacc[mt][t], 0, 0, 0);
+        }
+#pragma unroll
+        for (int mt = 0; mt < MTC; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int m = 16 * mt + 4 * krow + r;
+                const v4f v = {dacc[mt][0][r], dacc[mt][1][r], dacc[mt][2][r], dacc[mt][3][r]};
+                if (FAST) *reinterpret_cast<v4f *>(out + (size_t)m * p + e0 + 4 * col) = v;
+                else store_tile<true>(out + (size_t)m * p, (size_t)m * p, e0, col, p, a.d, v);
+            }
+        __syncthreads();                                  // LDS reused by the next block
+    }
+}
+
 // ---- K5: error norms ---------------------------------------------------------
 
 constexpr int kNormWorkers = 8;
@@ -1242,8 +1373,8 @@ void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, 
 
 template <int KS>
 void launch_decode_ks(const DecParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
-    if constexpr (KS >= 16 && KS <= 20) {
-        if (path == Path::kFast && a.MT == 4 && a.mt0 == 0 && a.mt1 == 4) {   // c = 64: double-buffered
+    if constexpr (KS == 18 || KS == 20) {                // c = 64: K = 63 + N >= 65 observations
+        if (path == Path::kFast && a.MT == 4 && a.mt0 == 0 && a.mt1 == 4) {   // double-buffered
             const size_t l = (size_t)4 * ((KS + 3) / 4) * 256 * sizeof(float) + (size_t)4 * KS * sizeof(float *);
             hipLaunchKernelGGL((k_decode_dbuf<KS, 4>), grid, dim3(kThreads), l, s, a);
             return;
@@ -1620,6 +1751,38 @@ void launch_fused(const FusedParams &a, const BlockSplit &bs, size_t lds, hipStr
                            dim3(threads), lds, s, f);
     }
 }
+// N in {2, 4, 8}: k_fused_lanes, N waves per workgroup.
+template <int MTC, int NW>
+int launch_fused_lanes(const FusedParams &a, const BlockSplit &bs, hipStream_t s) {
+    constexpr int C = 16 * MTC, K = C + NW - 1, KSD = (K + 3) / 4;
+    const size_t lds = sizeof(float) * (size_t)NW * std::max<size_t>((size_t)C * 64 + 8, (size_t)4 * KSD * 64 + 8);
+    if (lds > 160 * 1024) return fail(CERAR_E_INVAL, "N=%d, c=%d needs %zu bytes of LDS", NW, C, lds);
+    if (a.KSd != KSD) return fail(CERAR_E_INVAL, "decode K-steps %d != %d", a.KSd, KSD);
+    FusedParams f = a;
+    if (bs.interior > 0) {
+        f.blk0 = 0;
+        f.blk1 = bs.interior;
+        hipLaunchKernelGGL((k_fused_lanes<MTC, NW, true>), dim3((unsigned)std::min<size_t>(bs.interior, 2048)),
+                           dim3(64 * NW), lds, s, f);
+    }
+    if (bs.total > bs.interior) {
+        f.blk0 = bs.interior;
+        f.blk1 = bs.total;
+        hipLaunchKernelGGL((k_fused_lanes<MTC, NW, false>),
+                           dim3((unsigned)std::min<size_t>(bs.total - bs.interior, 2048)), dim3(64 * NW), lds, s, f);
+    }
+    return CERAR_OK;
+}
+
+template <int NW>
+int launch_fused_lanes_c(const FusedParams &a, const BlockSplit &bs, hipStream_t s) {
+    switch (a.c / 16) {
+        case 1: return launch_fused_lanes<1, NW>(a, bs, s);
+        case 2: return launch_fused_lanes<2, NW>(a, bs, s);
+        case 3: return launch_fused_lanes<3, NW>(a, bs, s);
+        default: return launch_fused_lanes<4, NW>(a, bs, s);
+    }
+}
 }  // namespace
 
 extern "C" int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
@@ -1659,7 +1822,11 @@ extern "C" int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const
     a.KSd = plan->KSd;
     const BlockSplit bs = split_blocks(plan, p, d, true);
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (N <= 8) {
+    if (N == 2 || N == 4 || N == 8) {
+        st = N == 2 ? launch_fused_lanes_c<2>(a, bs, s)
+                    : (N == 4 ? launch_fused_lanes_c<4>(a, bs, s) : launch_fused_lanes_c<8>(a, bs, s));
+        if (st) return st;
+    } else if (N <= 8) {
         switch (c / 16) {
             case 1: launch_fused<1, 512>(a, bs, lds, s); break;
             case 2: launch_fused<2, 512>(a, bs, lds, s); break;

@@ -118,6 +118,8 @@ CASES = [
     ("N8-c16-tail", 8, 16, 16 * 4096 + 9, "o_eps", 0.3),
     ("N8-c32", 8, 32, 32 * 2048, "kappa", 1e3),
     ("N8-c64-ragged", 8, 64, 64 * 1536 + 61, "kappa", 1e3),
+    ("N13-c64", 13, 64, 64 * 900 + 29, "kappa", 1e3),      # K = 76: the 20-K-step decode
+    ("N2-c64", 2, 64, 64 * 700, "o_eps", 0.3),             # K = 65: 17 K-steps padded to 18
     ("N16-c128", 16, 128, 128 * 320, "kappa", 1e3),
 ]
 
@@ -360,6 +362,10 @@ FUSED = [
     ("N16-c32", 16, 32, 32 * 640),
     ("N2-c48", 2, 48, 48 * 300 + 7),
     ("N8-c64-d1", 8, 64, 1),
+    # N not in {2, 4, 8}: the one-barrier-per-round kernel
+    ("N3-c16", 3, 16, 16 * 500 + 3),
+    ("N6-c64", 6, 64, 64 * 700 + 9),
+    ("N5-c48-tail", 5, 48, 48 * 129 + 47),
 ]
 
 
