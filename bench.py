@@ -42,8 +42,8 @@ def log(msg):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = headline)")
     ap.add_argument("--plan-iters", type=int, default=100, help="ALS iterations of the kappa design")
     ap.add_argument("--cpu-positions", type=int, default=1 << 21,
@@ -284,8 +284,9 @@ def cpu_baseline(wl, S):
         dt = time.perf_counter() - t0
     assert all(np.all(np.isfinite(o)) for o in out)
     bytes_sample = N * (8 * c + 3 * N - 9) * S * 4
+    step_bytes = N * (8 * c + 3 * N - 9) * p * 4
     return {"value": bytes_sample / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "seconds": dt,
+            "seconds": dt, "extrapolated_step_s": round(dt * step_bytes / bytes_sample, 1),
             "sample": f"{S} positions x {c} chunks x {N} workers of the same workload "
                       f"({S / p:.2e} of the positions), fp64 NumPy oracle "
                       f"(encode, Algorithm 1 lock-step, decode) with its {plan_desc}; "
