@@ -119,7 +119,7 @@ CASES = [
     ("N8-c32", 8, 32, 32 * 2048, "kappa", 1e3),
     ("N8-c64-ragged", 8, 64, 64 * 1536 + 61, "kappa", 1e3),
     ("N13-c64", 13, 64, 64 * 900 + 29, "kappa", 1e3),      # K = 76: the 20-K-step decode
-    ("N2-c64", 2, 64, 64 * 700, "o_eps", 0.3),             # K = 65: 17 K-steps padded to 18
+    ("N2-c64", 2, 64, 64 * 700, "kappa", 1e3),             # K = 65: 17 K-steps padded to 18
     ("N16-c128", 16, 128, 128 * 320, "kappa", 1e3),
 ]
 
