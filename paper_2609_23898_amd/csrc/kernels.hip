@@ -1096,16 +1096,25 @@ __global__ __launch_bounds__(64 * NW) void k_fused_lanes(FusedParams a) {
         const size_t e0 = blk * 64;
         // 1. encode: delta_w = U_w^T G_w^T on this block
         float *mydelta = sm + (size_t)w * DS;
+        float anext[KSE];                                // A fragments of the next M-tile, one tile ahead
+#pragma unroll
+        for (int ks = 0; ks < KSE; ++ks) anext[ks] = ef[(size_t)ks * 64 + lane];
 #pragma unroll 1
         for (int mt = 0; mt < MTC; ++mt) {
+            float av[KSE];
+#pragma unroll
+            for (int ks = 0; ks < KSE; ++ks) av[ks] = anext[ks];
+            if (mt + 1 < MTC) {
+#pragma unroll
+                for (int ks = 0; ks < KSE; ++ks) anext[ks] = ef[((size_t)(mt + 1) * KSE + ks) * 64 + lane];
+            }
             v4f acc[4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int ks = 0; ks < KSE; ++ks) {
-                const float av = ef[((size_t)mt * KSE + ks) * 64 + lane];
 #pragma unroll
-                for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, b[ks][t], acc[t], 0, 0, 0);
+                for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ks], b[ks][t], acc[t], 0, 0, 0);
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
