@@ -226,8 +226,10 @@ int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *gra
  * slots back to back (stride ld_work >= sum_b c*p_b); ws is
  * cerar_bucketed_workspace_bytes.  Enqueued on `stream`: every bucket's
  * encode, then each round as one launch for up to 64 buckets and all
- * workers, then every bucket's decode.  bucket_off/bucket_len are host
- * arrays; buckets may not overlap in out. */
+ * workers, then every bucket's decode.  With c <= 64 and 16-byte aligned
+ * rows in every bucket, the encode and the decode are batched as well (up to
+ * 32 buckets per launch); otherwise each bucket gets its own launches.
+ * bucket_off/bucket_len are host arrays; buckets may not overlap in out. */
 int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len,
                                    int nbuckets, size_t *work_floats, size_t *ws_bytes);
 int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,

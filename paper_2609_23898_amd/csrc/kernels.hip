@@ -15,6 +15,7 @@
 #include <cstdint>
 #include <map>
 #include <mutex>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -262,13 +263,61 @@ struct EncParams {
     size_t blk_per_wg;      // consecutive blocks each workgroup sweeps (a multiple of kWaves)
 };
 
+// Several independent instances of one plan (DDP buckets) in one launch:
+// instance q owns workgroups [wg0_q, wg0_{q+1}) of the grid and brings its
+// own buffers, chunk length and block range; the rest is shared.
+constexpr int kMaxInst = 32;
+
+// Index of the last instance whose first workgroup is at or before `block`.
+template <class Inst>
+__device__ inline int instance_of(const Inst *in, int n, unsigned block) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (in[mid].wg0 <= block) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+struct EncInst {
+    const float *grads;
+    size_t d;
+    float *work, *pool;
+    size_t p, pool_stride;
+    size_t blk0, blk1, blk_per_wg;
+    unsigned wg0;
+};
+
+struct EncBatch {
+    EncParams base;         // shared fields; the per-instance ones come from in[]
+    int n;
+    EncInst in[kMaxInst];
+    // this workgroup's parameters, and its block index within its instance
+    __device__ EncParams at(unsigned &bid) const {
+        const EncInst &I = in[instance_of(in, n, blockIdx.x)];
+        EncParams a = base;
+        a.grads = I.grads;
+        a.d = I.d;
+        a.sb.work = I.work;
+        a.sb.pool = I.pool;
+        a.sb.p = I.p;
+        a.sb.pool_stride = I.pool_stride;
+        a.blk0 = I.blk0;
+        a.blk1 = I.blk1;
+        a.blk_per_wg = I.blk_per_wg;
+        bid = blockIdx.x - I.wg0;
+        return a;
+    }
+};
+
 // FAST: interior blocks only (full rows, no masks, non-temporal 16-byte
 // accesses); otherwise the masked path for tails and the scalar layout.
 template <int KS, bool VEC, bool AREG, bool FAST>
-__global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
+__device__ __forceinline__ void k_encode_body(const EncParams &a, unsigned bid) {
     extern __shared__ float sfrag[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
+    const int worker = bid % a.N;           // workers interleaved across the grid
+    const int wg = bid / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int nmt = a.mt1 - a.mt0;
@@ -333,15 +382,25 @@ __global__ __launch_bounds__(kThreads) void k_encode(EncParams a) {
     }
 }
 
+template <int KS, bool VEC, bool AREG, bool FAST>
+__global__ __launch_bounds__(kThreads) void k_encode(EncParams a) { k_encode_body<KS, VEC, AREG, FAST>(a, blockIdx.x); }
+
+template <int KS, bool VEC, bool AREG, bool FAST>
+__global__ __launch_bounds__(kThreads) void k_encode_batch(EncBatch b) {
+    unsigned bid;
+    const EncParams a = b.at(bid);
+    k_encode_body<KS, VEC, AREG, FAST>(a, bid);
+}
+
 // Pipelined interior encode for c <= 64 (up to 4 M-tiles): the coefficients
 // stay in LDS, all M-tile accumulators stay in AGPRs, and the next block's
 // loads are issued before the current block's stores, so every wave keeps
 // loads in flight while its stores drain.
 template <int KS, int MTMAX, int NB>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_encode_pipe(EncParams a) {
+__device__ __forceinline__ void k_encode_pipe_body(const EncParams &a, unsigned bid) {
     extern __shared__ float sfrag[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
+    const int worker = bid % a.N;           // workers interleaved across the grid
+    const int wg = bid / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int MT = a.mt1 - a.mt0;                       // <= MTMAX
@@ -401,6 +460,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     }
 }
 
+template <int KS, int MTMAX, int NB>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_encode_pipe(EncParams a) { k_encode_pipe_body<KS, MTMAX, NB>(a, blockIdx.x); }
+
+template <int KS, int MTMAX, int NB>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_encode_pipe_batch(EncBatch b) {
+    unsigned bid;
+    const EncParams a = b.at(bid);
+    k_encode_pipe_body<KS, MTMAX, NB>(a, bid);
+}
+
 // Double-buffered interior encode for c = 16 MTC (up to 64): two register
 // buffers of float4 B operands, so block n+1's loads are in flight during all
 // of block n's MFMA work, and each M-tile's 16 output rows are stored as soon
@@ -411,10 +480,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 // back edge, and a header before the first tile made every other block wait
 // for all of the previous block's stores to drain.
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_dbuf(EncParams a) {
+__device__ __forceinline__ void k_encode_dbuf_body(const EncParams &a, unsigned bid) {
     extern __shared__ float sfrag[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
+    const int worker = bid % a.N;           // workers interleaved across the grid
+    const int wg = bid / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int KSx = a.KSe;
@@ -464,6 +533,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         blk = next;
         tile(b0, blk, 0);
     }
+}
+
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_dbuf(EncParams a) { k_encode_dbuf_body<KS, MTC>(a, blockIdx.x); }
+
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_dbuf_batch(EncBatch b) {
+    unsigned bid;
+    const EncParams a = b.at(bid);
+    k_encode_dbuf_body<KS, MTC>(a, bid);
 }
 
 // Wide encode for c = 16 MTC > 64: at 2c flops per byte the contraction is
@@ -607,13 +686,7 @@ struct BatchRoundParams {
 
 template <int MODE, bool VEC>
 __global__ __launch_bounds__(kRoundThreads) void k_round_batch(BatchRoundParams a) {
-    int lo = 0, hi = a.nb - 1;                       // last instance with wg0 <= blockIdx.x
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) / 2;
-        if (a.b[mid].wg0 <= blockIdx.x) lo = mid;
-        else hi = mid - 1;
-    }
-    const BatchInst q = a.b[lo];
+    const BatchInst q = a.b[instance_of(a.b, a.nb, blockIdx.x)];
     const unsigned local = blockIdx.x - q.wg0;
     const int worker = (int)(local / q.wgpw);
     const SlotBase sb{q.work, a.ld_work, q.p, q.pool, q.pool_stride, a.Nc, a.c};
@@ -636,11 +709,41 @@ struct DecParams {
     size_t blk_per_wg;
 };
 
+struct DecInst {
+    float *work, *pool;
+    size_t p, pool_stride;
+    float *out;
+    size_t d;
+    size_t blk0, blk1, blk_per_wg;
+    unsigned wg0;
+};
+
+struct DecBatch {
+    DecParams base;         // shared fields; the per-instance ones come from in[]
+    int n;
+    DecInst in[kMaxInst];
+    __device__ DecParams at(unsigned &bid) const {
+        const DecInst &I = in[instance_of(in, n, blockIdx.x)];
+        DecParams a = base;
+        a.sb.work = I.work;
+        a.sb.pool = I.pool;
+        a.sb.p = I.p;
+        a.sb.pool_stride = I.pool_stride;
+        a.out = I.out;
+        a.d = I.d;
+        a.blk0 = I.blk0;
+        a.blk1 = I.blk1;
+        a.blk_per_wg = I.blk_per_wg;
+        bid = blockIdx.x - I.wg0;
+        return a;
+    }
+};
+
 template <int KS, bool VEC, bool AREG, bool FAST>
-__global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
+__device__ __forceinline__ void k_decode_body(const DecParams &a, unsigned bid) {
     extern __shared__ float smem[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
+    const int worker = bid % a.N;           // workers interleaved across the grid
+    const int wg = bid / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int nmt = a.mt1 - a.mt0;
@@ -704,14 +807,24 @@ __global__ __launch_bounds__(kThreads) void k_decode(DecParams a) {
     }
 }
 
+template <int KS, bool VEC, bool AREG, bool FAST>
+__global__ __launch_bounds__(kThreads) void k_decode(DecParams a) { k_decode_body<KS, VEC, AREG, FAST>(a, blockIdx.x); }
+
+template <int KS, bool VEC, bool AREG, bool FAST>
+__global__ __launch_bounds__(kThreads) void k_decode_batch(DecBatch b) {
+    unsigned bid;
+    const DecParams a = b.at(bid);
+    k_decode_body<KS, VEC, AREG, FAST>(a, bid);
+}
+
 // Pipelined interior decode for c <= 64: same scheme, B rows through the
 // per-worker table of observation slots; NB adjacent blocks per wave when
 // the M-tiles are few (MTMAX <= 2), as in the encode.
 template <int KS, int MTMAX, int NB>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * NB <= 20 ? 3 : (KS * NB <= 32 ? 2 : 1)))) void k_decode_pipe(DecParams a) {
+__device__ __forceinline__ void k_decode_pipe_body(const DecParams &a, unsigned bid) {
     extern __shared__ float smem[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
+    const int worker = bid % a.N;           // workers interleaved across the grid
+    const int wg = bid / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int MT = a.mt1 - a.mt0;                       // <= MTMAX
@@ -772,14 +885,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * N
     }
 }
 
+template <int KS, int MTMAX, int NB>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * NB <= 20 ? 3 : (KS * NB <= 32 ? 2 : 1)))) void k_decode_pipe(DecParams a) { k_decode_pipe_body<KS, MTMAX, NB>(a, blockIdx.x); }
+
+template <int KS, int MTMAX, int NB>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * NB <= 20 ? 3 : (KS * NB <= 32 ? 2 : 1)))) void k_decode_pipe_batch(DecBatch b) {
+    unsigned bid;
+    const DecParams a = b.at(bid);
+    k_decode_pipe_body<KS, MTMAX, NB>(a, bid);
+}
+
 // Double-buffered interior decode for c = 16 MTC (up to 64), same scheme as
 // the double-buffered encode; the B rows come through the per-worker table of
 // observation slots.
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_dbuf(DecParams a) {
+__device__ __forceinline__ void k_decode_dbuf_body(const DecParams &a, unsigned bid) {
     extern __shared__ float smem[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
+    const int worker = bid % a.N;           // workers interleaved across the grid
+    const int wg = bid / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, krow = lane >> 4;
     const int KSx = a.KSd;
@@ -831,6 +954,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         blk = next;
         tile(b0, blk, 0);
     }
+}
+
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_dbuf(DecParams a) { k_decode_dbuf_body<KS, MTC>(a, blockIdx.x); }
+
+template <int KS, int MTC>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_dbuf_batch(DecBatch b) {
+    unsigned bid;
+    const DecParams a = b.at(bid);
+    k_decode_dbuf_body<KS, MTC>(a, bid);
 }
 
 // Wide decode for c = 16 MTC > 64, same scheme as the wide encode; the B
@@ -1350,14 +1483,56 @@ void wg_for(size_t nblk, int &wg_per_worker, size_t &blk_per_wg) {
 // Launch flavours: interior blocks (FAST), masked 16-byte layout, scalar layout.
 enum class Path { kFast, kMaskedVec, kScalar };
 
-template <int KS, bool AREG>
-void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+// The shared fields of a single-instance launch or of a batch table.
+const EncParams &shared_of(const EncParams &a) { return a; }
+const EncParams &shared_of(const EncBatch &a) { return a.base; }
+const DecParams &shared_of(const DecParams &a) { return a; }
+const DecParams &shared_of(const DecBatch &a) { return a.base; }
+
+template <class P>
+constexpr bool kIsBatch = std::is_same_v<P, EncBatch> || std::is_same_v<P, DecBatch>;
+
+// Each launcher starts the single-instance kernel, or its batch twin when
+// given a batch table.
+template <int KS, int MTMAX, int NB, class P>
+void go_encode_pipe(const P &a, dim3 g, size_t l, hipStream_t s) {
+    if constexpr (kIsBatch<P>) hipLaunchKernelGGL((k_encode_pipe_batch<KS, MTMAX, NB>), g, dim3(kThreads), l, s, a);
+    else hipLaunchKernelGGL((k_encode_pipe<KS, MTMAX, NB>), g, dim3(kThreads), l, s, a);
+}
+template <int KS, int MTC, class P>
+void go_encode_dbuf(const P &a, dim3 g, size_t l, hipStream_t s) {
+    if constexpr (kIsBatch<P>) hipLaunchKernelGGL((k_encode_dbuf_batch<KS, MTC>), g, dim3(kThreads), l, s, a);
+    else hipLaunchKernelGGL((k_encode_dbuf<KS, MTC>), g, dim3(kThreads), l, s, a);
+}
+template <int KS, bool VEC, bool AREG, bool FAST, class P>
+void go_encode(const P &a, dim3 g, size_t l, hipStream_t s) {
+    if constexpr (kIsBatch<P>) hipLaunchKernelGGL((k_encode_batch<KS, VEC, AREG, FAST>), g, dim3(kThreads), l, s, a);
+    else hipLaunchKernelGGL((k_encode<KS, VEC, AREG, FAST>), g, dim3(kThreads), l, s, a);
+}
+template <int KS, int MTMAX, int NB, class P>
+void go_decode_pipe(const P &a, dim3 g, size_t l, hipStream_t s) {
+    if constexpr (kIsBatch<P>) hipLaunchKernelGGL((k_decode_pipe_batch<KS, MTMAX, NB>), g, dim3(kThreads), l, s, a);
+    else hipLaunchKernelGGL((k_decode_pipe<KS, MTMAX, NB>), g, dim3(kThreads), l, s, a);
+}
+template <int KS, int MTC, class P>
+void go_decode_dbuf(const P &a, dim3 g, size_t l, hipStream_t s) {
+    if constexpr (kIsBatch<P>) hipLaunchKernelGGL((k_decode_dbuf_batch<KS, MTC>), g, dim3(kThreads), l, s, a);
+    else hipLaunchKernelGGL((k_decode_dbuf<KS, MTC>), g, dim3(kThreads), l, s, a);
+}
+template <int KS, bool VEC, bool AREG, bool FAST, class P>
+void go_decode(const P &a, dim3 g, size_t l, hipStream_t s) {
+    if constexpr (kIsBatch<P>) hipLaunchKernelGGL((k_decode_batch<KS, VEC, AREG, FAST>), g, dim3(kThreads), l, s, a);
+    else hipLaunchKernelGGL((k_decode<KS, VEC, AREG, FAST>), g, dim3(kThreads), l, s, a);
+}
+
+template <int KS, bool AREG, class P>
+void launch_encode_ks(const P &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+    const EncParams &sh = shared_of(a);
     if constexpr (AREG && KS >= 4) {
         if (path == Path::kFast) {
             if constexpr (KS == 16) {
-                if (a.MT == 4 && a.mt0 == 0 && a.mt1 == 4) {   // c = 64: double-buffered
-                    const size_t l = (size_t)4 * (KS / 4) * 256 * sizeof(float);
-                    hipLaunchKernelGGL((k_encode_dbuf<KS, 4>), grid, dim3(kThreads), l, s, a);
+                if (sh.MT == 4 && sh.mt0 == 0 && sh.mt1 == 4) {   // c = 64: double-buffered
+                    go_encode_dbuf<KS, 4>(a, grid, (size_t)4 * (KS / 4) * 256 * sizeof(float), s);
                     return;
                 }
             }
@@ -1365,44 +1540,44 @@ void launch_encode_ks(const EncParams &a, Path path, size_t lds, hipStream_t s, 
             // NB blocks per wave keep ~16 KB of loads in flight per wave at any c
             constexpr int MTMAX = KS <= 4 ? 1 : (KS <= 8 ? 2 : 4);
             constexpr int NB = KS <= 4 ? 4 : (KS <= 8 ? 2 : 1);
-            const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float);
-            hipLaunchKernelGGL((k_encode_pipe<KS, MTMAX, NB>), grid, dim3(kThreads), l, s, a);
+            go_encode_pipe<KS, MTMAX, NB>(a, grid, (size_t)(sh.mt1 - sh.mt0) * ((KS + 3) / 4) * 256 * sizeof(float), s);
             return;
         }
     }
     if constexpr (!AREG) {
         if (path == Path::kFast) {
-            hipLaunchKernelGGL((k_encode<KS, true, AREG, true>), grid, dim3(kThreads), lds, s, a);
+            go_encode<KS, true, AREG, true>(a, grid, lds, s);
             return;
         }
     }
-    if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_encode<KS, true, AREG, false>), grid, dim3(kThreads), lds, s, a);
-    else hipLaunchKernelGGL((k_encode<KS, false, AREG, false>), grid, dim3(kThreads), lds, s, a);
+    if (path == Path::kMaskedVec) go_encode<KS, true, AREG, false>(a, grid, lds, s);
+    else go_encode<KS, false, AREG, false>(a, grid, lds, s);
 }
 
-template <int KS>
-void launch_decode_ks(const DecParams &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+template <int KS, class P>
+void launch_decode_ks(const P &a, Path path, size_t lds, hipStream_t s, dim3 grid) {
+    const DecParams &sh = shared_of(a);
     if constexpr (KS == 18 || KS == 20) {                // c = 64: K = 63 + N >= 65 observations
-        if (path == Path::kFast && a.MT == 4 && a.mt0 == 0 && a.mt1 == 4) {   // double-buffered
-            const size_t l = (size_t)4 * ((KS + 3) / 4) * 256 * sizeof(float) + (size_t)4 * KS * sizeof(float *);
-            hipLaunchKernelGGL((k_decode_dbuf<KS, 4>), grid, dim3(kThreads), l, s, a);
+        if (path == Path::kFast && sh.MT == 4 && sh.mt0 == 0 && sh.mt1 == 4) {   // double-buffered
+            go_decode_dbuf<KS, 4>(a, grid, (size_t)4 * ((KS + 3) / 4) * 256 * sizeof(float) +
+                                               (size_t)4 * KS * sizeof(float *), s);
             return;
         }
     }
-    if (path == Path::kFast && a.mt1 - a.mt0 <= kMaxRegTiles) {
-        const size_t l = (size_t)(a.mt1 - a.mt0) * ((KS + 3) / 4) * 256 * sizeof(float) +
+    if (path == Path::kFast && sh.mt1 - sh.mt0 <= kMaxRegTiles) {
+        const size_t l = (size_t)(sh.mt1 - sh.mt0) * ((KS + 3) / 4) * 256 * sizeof(float) +
                          (size_t)4 * KS * sizeof(float *);
         if constexpr (KS <= 24) {
-            if (a.mt1 - a.mt0 <= 2) {             // c <= 32: fewer accumulators, two blocks per wave if short
-                hipLaunchKernelGGL((k_decode_pipe<KS, 2, (KS <= 8 ? 2 : 1)>), grid, dim3(kThreads), l, s, a);
+            if (sh.mt1 - sh.mt0 <= 2) {             // c <= 32: fewer accumulators, two blocks per wave if short
+                go_decode_pipe<KS, 2, (KS <= 8 ? 2 : 1)>(a, grid, l, s);
                 return;
             }
         }
-        hipLaunchKernelGGL((k_decode_pipe<KS, kMaxRegTiles, 1>), grid, dim3(kThreads), l, s, a);
+        go_decode_pipe<KS, kMaxRegTiles, 1>(a, grid, l, s);
     }
-    else if (path == Path::kFast) hipLaunchKernelGGL((k_decode<KS, true, false, true>), grid, dim3(kThreads), lds, s, a);
-    else if (path == Path::kMaskedVec) hipLaunchKernelGGL((k_decode<KS, true, false, false>), grid, dim3(kThreads), lds, s, a);
-    else hipLaunchKernelGGL((k_decode<KS, false, false, false>), grid, dim3(kThreads), lds, s, a);
+    else if (path == Path::kFast) go_decode<KS, true, false, true>(a, grid, lds, s);
+    else if (path == Path::kMaskedVec) go_decode<KS, true, false, false>(a, grid, lds, s);
+    else go_decode<KS, false, false, false>(a, grid, lds, s);
 }
 
 // M-tiles per launch so that their staged fragments fit the LDS budget.
@@ -1467,6 +1642,35 @@ int decode_ks(const DecParams &a, const BlockSplit &bs, size_t lds, hipStream_t 
     });
 }
 
+// Calls f with the compiled K-step count that covers ks: the register-tile
+// encode (c <= 64) and the decode.
+template <class F>
+void with_encode_ks(int ks, F f) {
+    if (ks <= 1) f(std::integral_constant<int, 1>{});
+    else if (ks <= 2) f(std::integral_constant<int, 2>{});
+    else if (ks <= 4) f(std::integral_constant<int, 4>{});
+    else if (ks <= 8) f(std::integral_constant<int, 8>{});
+    else f(std::integral_constant<int, 16>{});
+}
+
+template <class F>
+void with_decode_ks(int ks, F f) {
+    if (ks <= 4) f(std::integral_constant<int, 4>{});
+    else if (ks <= 8) f(std::integral_constant<int, 8>{});
+    else if (ks <= 10) f(std::integral_constant<int, 10>{});
+    else if (ks <= 12) f(std::integral_constant<int, 12>{});
+    else if (ks <= 16) f(std::integral_constant<int, 16>{});
+    else if (ks <= 18) f(std::integral_constant<int, 18>{});
+    else if (ks <= 20) f(std::integral_constant<int, 20>{});
+    else if (ks <= 24) f(std::integral_constant<int, 24>{});
+    else if (ks <= 32) f(std::integral_constant<int, 32>{});
+    else if (ks <= 36) f(std::integral_constant<int, 36>{});
+    else if (ks <= 40) f(std::integral_constant<int, 40>{});
+    else f(std::integral_constant<int, 48>{});
+}
+
+constexpr size_t kDecodeRowsBytes = (size_t)4 * kMaxDecodeKS * sizeof(float *) + 16;
+
 int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, size_t d,
                    const float *grads, size_t ld_grads, float *work, size_t ld_work, void *ws, hipStream_t s) {
     EncParams a;
@@ -1485,11 +1689,7 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     a.mt0 = 0;
     a.mt1 = plan->MT;
     if (plan->MT <= kMaxRegTiles) {                  // c <= 64: coefficients in registers
-        if (ks <= 1) encode_ks<1, true>(a, bs, 0, s, N);
-        else if (ks <= 2) encode_ks<2, true>(a, bs, 0, s, N);
-        else if (ks <= 4) encode_ks<4, true>(a, bs, 0, s, N);
-        else if (ks <= 8) encode_ks<8, true>(a, bs, 0, s, N);
-        else encode_ks<16, true>(a, bs, 0, s, N);
+        with_encode_ks(ks, [&](auto K) { encode_ks<decltype(K)::value, true>(a, bs, 0, s, N); });
     } else {
         // All M-tiles in one launch (c <= 128 fits the LDS budget), which an
         // in-place encode needs: every input row is read before any is written.
@@ -1574,7 +1774,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
     const bool vec = g.vec && (ld_out % 4 == 0) && aligned16(out);
     const BlockSplit bs = split_blocks(plan, g.p, d, vec);
     const int N = plan->N, ks = plan->KSd;
-    const size_t rows_bytes = (size_t)4 * kMaxDecodeKS * sizeof(float *) + 16;
+    const size_t rows_bytes = kDecodeRowsBytes;
     BlockSplit rest = bs;
     if (plan->c == 128 && bs.interior > 0 && ks <= 48) {
         // c = 128: interior blocks on the wide kernel (all 8 M-tiles, one pass
@@ -1600,18 +1800,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
         a.mt0 = mt0;
         a.mt1 = std::min(plan->MT, mt0 + step);
         const size_t lds = (size_t)(a.mt1 - a.mt0) * ((ks + 3) / 4) * 256 * sizeof(float) + rows_bytes;
-        if (ks <= 4) decode_ks<4>(a, rest, lds, s, N);
-        else if (ks <= 8) decode_ks<8>(a, rest, lds, s, N);
-        else if (ks <= 10) decode_ks<10>(a, rest, lds, s, N);
-        else if (ks <= 12) decode_ks<12>(a, rest, lds, s, N);
-        else if (ks <= 16) decode_ks<16>(a, rest, lds, s, N);
-        else if (ks <= 18) decode_ks<18>(a, rest, lds, s, N);
-        else if (ks <= 20) decode_ks<20>(a, rest, lds, s, N);
-        else if (ks <= 24) decode_ks<24>(a, rest, lds, s, N);
-        else if (ks <= 32) decode_ks<32>(a, rest, lds, s, N);
-        else if (ks <= 36) decode_ks<36>(a, rest, lds, s, N);
-        else if (ks <= 40) decode_ks<40>(a, rest, lds, s, N);
-        else decode_ks<48>(a, rest, lds, s, N);
+        with_decode_ks(ks, [&](auto K) { decode_ks<decltype(K)::value>(a, rest, lds, s, N); });
         HIP_TRY(hipGetLastError(), "launch decode");
     }
     return CERAR_OK;
@@ -1914,6 +2103,133 @@ int bucket_layout(const cerar_plan *plan, int nb, const size_t *len, std::vector
     return CERAR_OK;
 }
 
+// Kernel arguments are limited to 4 KiB.
+static_assert(sizeof(EncBatch) <= 4096 && sizeof(DecBatch) <= 4096, "batch tables must fit the kernel arguments");
+
+// One bucket's share of a batched encode or decode: its buffers and geometry.
+struct BucketRef {
+    const float *grads;      // encode input (bucket offset applied)
+    float *out;              // decode output (bucket offset applied)
+    float *work;
+    void *ws;
+    size_t d, p, pool_stride;
+};
+
+// Every bucket's interior blocks in as few launches as kMaxInst allows, then
+// every bucket's tail blocks (masked kernels) the same way.  Set(batch, q,
+// bucket, blk0, blk1) fills instance q; Launch(batch, path, grid) starts it.
+template <class Batch, class Set, class Launch>
+int launch_bucket_batches(const cerar_plan *plan, const std::vector<BucketRef> &bk, Batch &b, Set set,
+                          Launch launch) {
+    const size_t N = plan->N;
+    for (int pass = 0; pass < 2; ++pass) {
+        b.n = 0;
+        size_t wgs = 0;
+        auto flush = [&]() -> int {
+            if (b.n == 0) return CERAR_OK;
+            if (wgs > 0x7fffffffu) return fail(CERAR_E_INVAL, "bucket batch too large for one launch");
+            launch(b, pass == 0 ? Path::kFast : Path::kMaskedVec, dim3((unsigned)wgs));
+            HIP_TRY(hipGetLastError(), "launch bucket batch");
+            b.n = 0;
+            wgs = 0;
+            return CERAR_OK;
+        };
+        for (size_t q = 0; q < bk.size(); ++q) {
+            const BlockSplit bs = split_blocks(plan, bk[q].p, bk[q].d, true);
+            const size_t lo = pass == 0 ? 0 : bs.interior, hi = pass == 0 ? bs.interior : bs.total;
+            if (hi <= lo) continue;
+            int wgpw;
+            size_t bpw;
+            wg_for(hi - lo, wgpw, bpw);
+            set(b, b.n, bk[q], lo, hi, bpw);
+            b.in[b.n].wg0 = (unsigned)wgs;
+            ++b.n;
+            wgs += N * (size_t)wgpw;
+            if (b.n == kMaxInst) {
+                const int st = flush();
+                if (st) return st;
+            }
+        }
+        const int st = flush();
+        if (st) return st;
+    }
+    return CERAR_OK;
+}
+
+int enqueue_encode_buckets(const cerar_plan *plan, const DeviceCopy *dc, const std::vector<BucketRef> &bk,
+                           size_t ld_grads, size_t ld_work, hipStream_t s) {
+    EncBatch b;
+    EncParams &a = b.base;
+    a = EncParams{};
+    a.ld_g = ld_grads;
+    a.sb = SlotBase{nullptr, ld_work, 0, nullptr, 0, plan->N * plan->c, plan->c};
+    a.frag = dc->enc_frag;
+    a.N = plan->N;
+    a.c = plan->c;
+    a.MT = plan->MT;
+    a.KSe = plan->KSe;
+    a.mt0 = 0;
+    a.mt1 = plan->MT;
+    auto set = [](EncBatch &x, int q, const BucketRef &r, size_t lo, size_t hi, size_t bpw) {
+        EncInst &I = x.in[q];
+        I.grads = r.grads;
+        I.d = r.d;
+        I.work = r.work;
+        I.pool = (float *)r.ws;
+        I.p = r.p;
+        I.pool_stride = r.pool_stride;
+        I.blk0 = lo;
+        I.blk1 = hi;
+        I.blk_per_wg = bpw;
+    };
+    int st = CERAR_OK;
+    with_encode_ks(plan->KSe, [&](auto K) {
+        st = launch_bucket_batches(plan, bk, b, set, [&](const EncBatch &x, Path path, dim3 grid) {
+            launch_encode_ks<decltype(K)::value, true>(x, path, 0, s, grid);
+        });
+    });
+    return st;
+}
+
+int enqueue_decode_buckets(const cerar_plan *plan, const DeviceCopy *dc, const std::vector<BucketRef> &bk,
+                           size_t ld_work, size_t ld_out, hipStream_t s) {
+    DecBatch b;
+    DecParams &a = b.base;
+    a = DecParams{};
+    a.sb = SlotBase{nullptr, ld_work, 0, nullptr, 0, plan->N * plan->c, plan->c};
+    a.ycols = dc->ycols;
+    a.ld_o = ld_out;
+    a.frag = dc->dec_frag;
+    a.N = plan->N;
+    a.c = plan->c;
+    a.K = plan->L + 1;
+    a.MT = plan->MT;
+    a.KSd = plan->KSd;
+    a.mt0 = 0;
+    a.mt1 = plan->MT;
+    const int ks = plan->KSd;
+    const size_t lds = (size_t)plan->MT * ((ks + 3) / 4) * 256 * sizeof(float) + kDecodeRowsBytes;
+    auto set = [](DecBatch &x, int q, const BucketRef &r, size_t lo, size_t hi, size_t bpw) {
+        DecInst &I = x.in[q];
+        I.work = r.work;
+        I.pool = (float *)r.ws;
+        I.p = r.p;
+        I.pool_stride = r.pool_stride;
+        I.out = r.out;
+        I.d = r.d;
+        I.blk0 = lo;
+        I.blk1 = hi;
+        I.blk_per_wg = bpw;
+    };
+    int st = CERAR_OK;
+    with_decode_ks(ks, [&](auto K) {
+        st = launch_bucket_batches(plan, bk, b, set, [&](const DecBatch &x, Path path, dim3 grid) {
+            launch_decode_ks<decltype(K)::value>(x, path, lds, s, grid);
+        });
+    });
+    return st;
+}
+
 }  // namespace
 
 extern "C" int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len, int nbuckets,
@@ -1968,8 +2284,20 @@ extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets
         all_vec = all_vec && g.vec;
     }
     // every bucket's encode, then each round once for all buckets (up to
-    // kMaxBatch per launch), then every bucket's decode: one stream orders them
-    for (int b = 0; b < nbuckets && !st; ++b)
+    // kMaxBatch per launch), then every bucket's decode: one stream orders them.
+    // With c <= 64 and 16-byte rows everywhere, the encode and the decode are
+    // batched too (interior blocks of up to kMaxInst buckets per launch, then
+    // their tails); otherwise each bucket gets its own launches.
+    bool batched = all_vec && plan->MT <= kMaxRegTiles && ld_grads % 4 == 0 && ld_out % 4 == 0 &&
+                   mtiles_per_launch(plan->MT, plan->KSd, kDecodeRowsBytes) == plan->MT;
+    std::vector<BucketRef> bk(nbuckets);
+    for (int b = 0; b < nbuckets; ++b) {
+        bk[b] = BucketRef{grads + bucket_off[b], out + bucket_off[b], work + lay[b].work_off,
+                          (char *)ws + lay[b].ws_off, bucket_len[b], lay[b].p, lay[b].stride};
+        batched = batched && aligned16(bk[b].grads) && aligned16(bk[b].out);
+    }
+    if (batched) st = enqueue_encode_buckets(plan, dc, bk, ld_grads, ld_work, s);
+    for (int b = 0; b < nbuckets && !st && !batched; ++b)
         st = enqueue_encode(plan, dc, geo[b], bucket_len[b], grads + bucket_off[b], ld_grads, work + lay[b].work_off,
                             ld_work, (char *)ws + lay[b].ws_off, s);
     for (int k = 1; k < plan->L && !st; ++k) {
@@ -2007,7 +2335,8 @@ extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets
             HIP_TRY(hipGetLastError(), "launch bucket round");
         }
     }
-    for (int b = 0; b < nbuckets && !st; ++b)
+    if (batched && !st) st = enqueue_decode_buckets(plan, dc, bk, ld_work, ld_out, s);
+    for (int b = 0; b < nbuckets && !st && !batched; ++b)
         st = enqueue_decode(plan, dc, geo[b], bucket_len[b], work + lay[b].work_off, ld_work,
                             (char *)ws + lay[b].ws_off, out + bucket_off[b], ld_out, s);
     return st;

@@ -342,6 +342,42 @@ def test_bucketed_matches_independent_instances():
         assert max_rel_l2(gpu[:, off:off + ln], ref) < 1e-4
 
 
+def _bucket_list(rng, nb, c):
+    """nb buckets, back to back, 16-byte aligned: c*32*k - 4*j floats, so
+    that most have interior blocks and a ragged last chunk row."""
+    lens = [int(c * 32 * rng.integers(1, 40) - 4 * rng.integers(0, 8)) for _ in range(nb)]
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).tolist()
+    return [(int(o), int(n)) for o, n in zip(offs, lens)]
+
+
+@pytest.mark.parametrize("N,c,nb,kind", [(8, 16, 40, "o_eps"), (4, 64, 5, "kappa"), (3, 20, 6, "o_eps"),
+                                         (8, 32, 33, "kappa")])
+def test_bucketed_batched_encode_and_decode(N, c, nb, kind):
+    """16-byte aligned buckets take the batched encode/decode (up to 32 buckets
+    per launch, interior blocks then tails); every bucket must match its own
+    oracle instance."""
+    torch, dev = torch_dev()
+    rng = np.random.default_rng(N * 100 + c)
+    buckets = _bucket_list(rng, nb, c)
+    buckets.append((buckets[-1][0] + buckets[-1][1], 4))          # a bucket of one position per chunk row
+    d = buckets[-1][0] + buckets[-1][1]
+    U, R = case_plan(N, c, kind, 0.3 if kind == "o_eps" else 1e3)
+    kappa = OP.max_kappa_M(U)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=N + c + nb)
+    work_floats, ws_bytes = plan.bucketed_sizes([b[1] for b in buckets])
+    work = torch.empty((N, work_floats), dtype=torch.float32, device=dev)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.full((N, d), float("nan"), dtype=torch.float32, device=dev)
+    C.ring_simulate_bucketed(plan, buckets, to_device(g), work, ws, out)
+    sync()
+    gpu = out.double().cpu().numpy()
+    assert np.all(np.isfinite(gpu))
+    for off, ln in buckets:
+        ref = oracle_allreduce(g[:, off:off + ln], U, R)
+        assert max_rel_l2(gpu[:, off:off + ln], ref) <= gate(kappa), (off, ln)
+
+
 def test_copy_kernel():
     torch, dev = torch_dev()
     for n in (1, 7, 4096, 1_000_003):
