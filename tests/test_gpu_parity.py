@@ -426,10 +426,13 @@ def test_fused_variant_matches_oracle_and_ring(name, N, c, d):
     ref = oracle_allreduce(g, U, R)
     kappa = OP.max_kappa_M(U)
     parity = max_rel_l2(fused, ref)
-    print(f"fused {name}: kappa_M={kappa:.3g} parity={parity:.3g}")
+    print(f"fused {name}: kappa_M={kappa:.3g} parity={parity:.3g} max|fused - ring|={np.abs(fused - ring).max():.3g}")
     assert np.all(np.isfinite(fused))
     assert parity <= gate(kappa)
-    assert max_rel_l2(fused, ring) <= 1e-5           # same arithmetic up to rounding order
+    # the fused kernels apply the ring's fp32 operations in the ring's order
+    # (MFMA K-steps in order, (recv - delta) + delta in the rounds), so the
+    # results are bit-identical, not just close
+    np.testing.assert_array_equal(fused, ring)
 
 
 def test_fused_variant_rejects_unsupported_shapes():
