@@ -180,10 +180,13 @@ int cerar_slot_map(const cerar_plan *plan, int step, int *slots);
  * work:   device, N slices of >= c*p floats at stride ld_work; may equal
  *         grads (in-place encode, the paper's storage discipline) when
  *         ld_work == ld_grads.
- * ws:     device, cerar_workspace_bytes(plan, d).
- * Steps must run in order 0, 1, .., L on the same (work, ws): the library
- * keeps the next expected step per workspace address and returns E_STATE
- * otherwise (step 0 is always accepted and restarts the sequence). */
+ * ws:     device, cerar_workspace_bytes(plan, d); may not overlap grads or
+ *         work, and grads may overlap work only by being the same buffer
+ *         (E_INVAL otherwise).
+ * Steps must run in order 0, 1, .., L on the same (work, ws) with the same
+ * d: the library keeps the next expected step and the encode's d per
+ * workspace address and returns E_STATE otherwise (step 0 is always accepted
+ * and restarts the sequence). */
 int cerar_encode_round(const cerar_plan *plan, int step, size_t d,
                        const float *grads, size_t ld_grads,
                        float *work, size_t ld_work, void *ws, cerar_stream stream);
@@ -192,7 +195,7 @@ int cerar_encode_round(const cerar_plan *plan, int step, size_t d,
  * read from the slots the ownership table names after round L.  Writes the
  * first d floats of out[i*ld_out ..] for every worker; nothing beyond d.
  * out must not overlap work or ws.  E_STATE unless rounds 1..L completed
- * on this workspace. */
+ * on this workspace with the same d. */
 int cerar_decode(const cerar_plan *plan, size_t d, const float *work, size_t ld_work,
                  const void *ws, float *out, size_t ld_out, cerar_stream stream);
 

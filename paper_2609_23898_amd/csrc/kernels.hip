@@ -1435,9 +1435,15 @@ int device_copy(const cerar_plan *plan, const DeviceCopy **out) {
     return CERAR_OK;
 }
 
-// Next expected step per workspace (cerar_encode_round ordering).
+// Next expected step per workspace (cerar_encode_round ordering), with the
+// plan and the gradient length the workspace's encode used.
+struct Cursor {
+    const cerar_plan *plan;
+    int next;
+    size_t d;
+};
 std::mutex g_cursor_mu;
-std::map<const void *, std::pair<const cerar_plan *, int>> g_cursor;
+std::map<const void *, Cursor> g_cursor;
 
 bool aligned16(const void *ptr) { return ((uintptr_t)ptr & 15) == 0; }
 
@@ -1460,6 +1466,10 @@ int check_common(const cerar_plan *plan, size_t d, const void *work, size_t ld_w
     if (st) return st;
     if (ld_work < (size_t)plan->c * g.p)
         return fail(CERAR_E_INVAL, "ld_work=%zu < c*p=%zu", ld_work, (size_t)plan->c * g.p);
+    const size_t N = plan->N;
+    if (overlap(work, ((N - 1) * ld_work + plan->c * g.p) * sizeof(float), ws,
+                (size_t)plan->tab.pool_slots() * g.pool_stride * sizeof(float)))
+        return fail(CERAR_E_INVAL, "work and ws overlap");
     g.vec = (g.p % 4 == 0) && (ld_work % 4 == 0) && aligned16(work) && aligned16(ws);
     return CERAR_OK;
 }
@@ -1807,7 +1817,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
 }
 
 int check_grads(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads, const float *work,
-                size_t ld_work, const Geometry &g) {
+                size_t ld_work, const void *ws, const Geometry &g) {
     if (!grads) return fail(CERAR_E_INVAL, "grads is NULL");
     if (ld_grads < d) return fail(CERAR_E_INVAL, "ld_grads=%zu < d=%zu", ld_grads, d);
     const size_t N = plan->N;
@@ -1817,6 +1827,9 @@ int check_grads(const cerar_plan *plan, size_t d, const float *grads, size_t ld_
                        ((N - 1) * ld_work + plan->c * g.p) * sizeof(float))) {
         return fail(CERAR_E_INVAL, "grads and work overlap without being the same buffer");
     }
+    if (overlap(grads, ((N - 1) * ld_grads + d) * sizeof(float), ws,
+                (size_t)plan->tab.pool_slots() * g.pool_stride * sizeof(float)))
+        return fail(CERAR_E_INVAL, "grads and ws overlap");
     return CERAR_OK;
 }
 
@@ -1849,7 +1862,7 @@ void release_device(cerar_plan *plan) {
     plan->dev.clear();
     std::lock_guard<std::mutex> c(g_cursor_mu);
     for (auto it = g_cursor.begin(); it != g_cursor.end();)
-        it = it->second.first == plan ? g_cursor.erase(it) : std::next(it);
+        it = it->second.plan == plan ? g_cursor.erase(it) : std::next(it);
 }
 
 }  // namespace cerar
@@ -1864,14 +1877,16 @@ extern "C" int cerar_encode_round(const cerar_plan *plan, int step, size_t d, co
     if (st) return st;
     if (step < 0 || step > plan->L) return fail(CERAR_E_INVAL, "step %d outside [0, L=%d]", step, plan->L);
     if (step == 0) {
-        st = check_grads(plan, d, grads, ld_grads, work, ld_work, g);
+        st = check_grads(plan, d, grads, ld_grads, work, ld_work, ws, g);
         if (st) return st;
     }
     {
         std::lock_guard<std::mutex> lk(g_cursor_mu);
         auto it = g_cursor.find(ws);
-        if (step > 0 && (it == g_cursor.end() || it->second.first != plan || it->second.second != step))
+        if (step > 0 && (it == g_cursor.end() || it->second.plan != plan || it->second.next != step))
             return fail(CERAR_E_STATE, "step %d called out of order on this workspace", step);
+        if (step > 0 && it->second.d != d)
+            return fail(CERAR_E_STATE, "step %d with d=%zu on a workspace encoded with d=%zu", step, d, it->second.d);
     }
     const DeviceCopy *dc;
     st = device_copy(plan, &dc);
@@ -1881,7 +1896,7 @@ extern "C" int cerar_encode_round(const cerar_plan *plan, int step, size_t d, co
                    : enqueue_round(plan, dc, g, step, work, ld_work, ws, s);
     if (st) return st;
     std::lock_guard<std::mutex> lk(g_cursor_mu);
-    g_cursor[ws] = {plan, step + 1};
+    g_cursor[ws] = Cursor{plan, step + 1, d};
     return CERAR_OK;
 }
 
@@ -1896,8 +1911,10 @@ extern "C" int cerar_decode(const cerar_plan *plan, size_t d, const float *work,
     {
         std::lock_guard<std::mutex> lk(g_cursor_mu);
         auto it = g_cursor.find(ws);
-        if (it == g_cursor.end() || it->second.first != plan || it->second.second != plan->L + 1)
+        if (it == g_cursor.end() || it->second.plan != plan || it->second.next != plan->L + 1)
             return fail(CERAR_E_STATE, "decode before rounds 1..L completed on this workspace");
+        if (it->second.d != d)
+            return fail(CERAR_E_STATE, "decode with d=%zu on a workspace encoded with d=%zu", d, it->second.d);
     }
     const DeviceCopy *dc;
     st = device_copy(plan, &dc);
@@ -1912,7 +1929,7 @@ extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float
     Geometry g;
     int st = check_common(plan, d, work, ld_work, ws, g);
     if (st) return st;
-    st = check_grads(plan, d, grads, ld_grads, work, ld_work, g);
+    st = check_grads(plan, d, grads, ld_grads, work, ld_work, ws, g);
     if (st) return st;
     st = check_out(plan, d, work, ld_work, ws, out, ld_out, g);
     if (st) return st;
@@ -1925,7 +1942,7 @@ extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float
     if (!st) st = enqueue_decode(plan, dc, g, d, work, ld_work, ws, out, ld_out, s);
     if (st) return st;
     std::lock_guard<std::mutex> lk(g_cursor_mu);
-    g_cursor[ws] = {plan, plan->L + 1};
+    g_cursor[ws] = Cursor{plan, plan->L + 1, d};
     return CERAR_OK;
 }
 

@@ -242,6 +242,13 @@ def test_device_calls_validate_before_touching_the_device():
     # grads and work overlapping without being equal
     assert lib.cerar_encode_round(plan.handle, 0, 4096, fake, 4096, ctypes.c_void_p(0x100000 + 64), 4096, ws,
                                   None) == -1
+    # work overlapping ws, grads overlapping ws
+    assert lib.cerar_encode_round(plan.handle, 0, 4096, fake, 4096, fake, 4096, ctypes.c_void_p(0x100000 + 256),
+                                  None) == -1
+    assert b"work and ws overlap" in lib.cerar_last_error()
+    assert lib.cerar_encode_round(plan.handle, 0, 4096, ctypes.c_void_p(0x5000000), 4096, fake, 4096,
+                                  ctypes.c_void_p(0x5000000 + 512), None) == -1
+    assert b"grads and ws overlap" in lib.cerar_last_error()
     # step out of range and out of order
     assert lib.cerar_encode_round(plan.handle, 7, 4096, fake, 4096, fake, 4096, ws, None) == -1
     assert lib.cerar_encode_round(plan.handle, 3, 4096, fake, 4096, fake, 4096, ws, None) == -6

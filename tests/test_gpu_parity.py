@@ -293,8 +293,14 @@ def test_step_order_enforced_on_device_buffers():
     assert ei.value.status == -6
     with pytest.raises(C.CerarError):
         C.decode(plan, d, work, ws, out)
+    with pytest.raises(C.CerarError) as ei:                # a round with another length
+        C.encode_round(plan, 1, d - 5, grads, work, ws)
+    assert ei.value.status == -6
     for k in range(1, c + N - 1):
         C.encode_round(plan, k, d, grads, work, ws)
+    with pytest.raises(C.CerarError) as ei:                # a decode with another length
+        C.decode(plan, d - 5, work, ws, out)
+    assert ei.value.status == -6
     C.decode(plan, d, work, ws, out)
     sync()
 
