@@ -119,7 +119,7 @@ CASES = [
     ("N8-c32", 8, 32, 32 * 2048, "kappa", 1e3),
     ("N8-c64-ragged", 8, 64, 64 * 1536 + 61, "kappa", 1e3),
     ("N13-c64", 13, 64, 64 * 900 + 29, "kappa", 1e3),      # K = 76: the 20-K-step decode
-    ("N2-c64", 2, 64, 64 * 700, "kappa", 1e3),             # K = 65: 17 K-steps padded to 18
+    ("N2-c64", 2, 64, 64 * 700, "kappa", 5e2),             # K = 65: 17 K-steps padded to 18
     ("N16-c128", 16, 128, 128 * 320, "kappa", 1e3),
 ]
 
@@ -149,11 +149,17 @@ def test_ring_simulate_parity(name, N, c, d, kind, param):
     ref = oracle_allreduce(g, U, R)
     S = OR.exact_sum(g)
     parity = max_rel_l2(gpu, ref)
+    # diagnostic: the oracle on the fp32-rounded coefficients the kernels use,
+    # which leaves only the kernels' own arithmetic in the difference
+    U32c, R32c = U.astype(np.float32).astype(np.float64), R.astype(np.float32).astype(np.float64)
+    parity32 = max_rel_l2(gpu, oracle_allreduce(g, U32c, R32c))
     err_gpu = max(rel_l2(gpu[i], S) for i in range(N))
     err_orc = max(rel_l2(ref[i], S) for i in range(N))
-    print(f"{name}: kappa_M={kappa:.3g} parity={parity:.3g} err_gpu={err_gpu:.4g} err_oracle={err_orc:.4g}")
+    print(f"{name}: kappa_M={kappa:.3g} parity={parity:.3g} parity_vs_fp32_coefficients={parity32:.3g} "
+          f"err_gpu={err_gpu:.4g} err_oracle={err_orc:.4g}")
     assert np.all(np.isfinite(gpu))
     assert parity <= gate(kappa)
+    assert parity32 <= gate(kappa)
     if kappa <= 1e3:
         assert abs(err_gpu - err_orc) <= 1e-4
     if kind == "o_eps" and param == 0.0:
