@@ -40,11 +40,13 @@ def log(msg):
 
 
 def parse():
+    from paper_2609_23898_amd import synth
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=4, help="workload 1..5 (4 = headline)")
+    ap.add_argument("--workload", default=synth.HEADLINE, choices=synth.WORKLOADS,
+                    help="synthetic workload (default: the headline, pythia-1.4b)")
     ap.add_argument("--plan-iters", type=int, default=100, help="ALS iterations of the kappa design")
     ap.add_argument("--cpu-positions", type=int, default=1 << 21,
                     help="positions of the bounded oracle sample (0 = skip cpu_baseline)")
@@ -100,7 +102,7 @@ def _step_bytes_cfg4():
     """Algorithmic bytes per launch of each family at the Pythia-1.4B workload."""
     from paper_2609_23898_amd import cerar as C
     from paper_2609_23898_amd import synth
-    wl = synth.workload(4)
+    wl = synth.workload("pythia-1.4b")
     N, c = wl.N, wl.c
     p = -(-wl.d // c)                            # a multiple of 32 here: the library's p too
     bw = C.phase_bytes_per_worker(N, c, p)
@@ -303,7 +305,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs the single-GPU simulation of all N workers; --gpus {args.gpus} is not "
-              "supported (multi-GPU CERAR is not part of this build)", file=sys.stderr)
+              "supported (this implementation runs all workers on one GPU)", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
@@ -314,7 +316,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     dev = "cuda:0"
-    wl = synth.workload(args.config)
+    wl = synth.workload(args.workload)
     N, c, d = wl.N, wl.c, wl.d
     t = time.perf_counter()
     plan, plan_desc = product_plan(C, wl, args.plan_iters)
@@ -480,7 +482,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
                      # the committed counter summary covers the headline workload only
-                     "traffic": committed_traffic(dominant) if args.config == 4 else None},
+                     "traffic": committed_traffic(dominant) if args.workload == synth.HEADLINE else None},
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
         "bucketed": bucketed,

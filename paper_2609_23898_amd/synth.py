@@ -290,22 +290,26 @@ def node_permutations(seed, count, c):
     return perms
 
 
-def workload(cfg):
-    """The five synthetic workloads, by number (1..5)."""
-    if cfg == 1:
+WORKLOADS = ("tiny-n4-c4", "iid-n8-c16-16m", "gpt2-small", "pythia-1.4b", "heavytail-n16-c128")
+HEADLINE = "pythia-1.4b"
+
+
+def workload(name):
+    """The synthetic workloads, by name (WORKLOADS)."""
+    if name == "tiny-n4-c4":
         return Workload("tiny N=4 c=4 d=4096 iid N(0,1)", 4, 4, 4096, seed=1)
-    if cfg == 2:
+    if name == "iid-n8-c16-16m":
         return Workload("N=8 c=16 d=2^24 iid N(0,1e-6)", 8, 16, 1 << 24, seed=2, scale=1e-3)
-    if cfg == 3:
+    if name == "gpt2-small":
         sizes = gpt2_small_tensor_sizes()
         return Workload("GPT-2-small N=8 c=32 d=124439808 lognormal tensors, 25MiB buckets",
                         8, 32, sum(sizes), seed=3, tensor_sizes=sizes,
                         buckets=ddp_buckets(sizes))
-    if cfg == 4:
+    if name == "pythia-1.4b":
         sizes = pythia_1_4b_tensor_sizes()
         return Workload("Pythia-1.4B N=8 c=64 d=1414647808 lognormal tensors",
                         8, 64, sum(sizes), seed=4, tensor_sizes=sizes)
-    if cfg == 5:
+    if name == "heavytail-n16-c128":
         return Workload("N=16 c=128 d=4e8 iid N(0,1), 1% x100 outliers", 16, 128,
                         400_000_000, seed=5, outlier_prob=0.01, outlier_factor=100.0)
-    raise ValueError(cfg)
+    raise ValueError(f"unknown workload {name!r}; one of {WORKLOADS}")

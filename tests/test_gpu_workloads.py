@@ -117,11 +117,11 @@ def _return_device_memory():
     torch.cuda.empty_cache()
 
 
-def test_workload2_o_eps():
+def test_iid_n8_c16_o_eps():
     """N=8, c=16, d=2^24, O(eps=1e-3): a quarter of the positions (2^18 of
     2^20); kappa(M) ~ 4e5, so parity is held to the kappa-scaled bound."""
     torch, dev = torch_dev()
-    wl = synth.workload(2)
+    wl = synth.workload("iid-n8-c16-16m")
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
     U, R = OP.mpc_plan(B, OP.o_eps_perturbation(np.diag(OP.chebyshev_nodes(wl.c)), 1e-3))
     kappa = OP.max_kappa_M(U)
@@ -131,17 +131,17 @@ def test_workload2_o_eps():
     run_stepwise(plan, wl.d, grads, work, ws, out)
     torch.cuda.synchronize()
     p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
-    parity, err_gpu, err_orc = check_sampled("workload2", wl, U, R, grads, out,
+    parity, err_gpu, err_orc = check_sampled("iid-n8-c16-16m", wl, U, R, grads, out,
                                              sample_positions(p, 1 << 18, 2), kappa)
     # the O(eps) error is the plan's, not the arithmetic's: eq. (14) bounds Phi
     assert err_orc < 1e-2
 
 
-def test_workload3_gpt2_buckets():
+def test_gpt2_small_buckets():
     """N=8, c=32, GPT-2-small gradient in 17 DDP buckets, kappa_max = 1e3:
     the bucketed call, 2048 sampled positions per bucket."""
     torch, dev = torch_dev()
-    wl = synth.workload(3)
+    wl = synth.workload("gpt2-small")
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
     U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(wl.c)), 0.3, 1e3, 20, order="projected")
     kappa = OP.max_kappa_M(U)
@@ -157,15 +157,15 @@ def test_workload3_gpt2_buckets():
     assert not bool(torch.isnan(out).any())            # every bucket wrote all of its d_b outputs
     for bi, (off, ln) in enumerate(wl.buckets):
         p = OR.chunk_len(ln, wl.c, CHUNK_ALIGN)
-        check_sampled(f"workload3 bucket {bi} (len {ln})", wl, U, R, grads, out,
+        check_sampled(f"gpt2-small bucket {bi} (len {ln})", wl, U, R, grads, out,
                       sample_positions(p, 2048, 300 + bi), kappa, off=off, length=ln)
 
 
-def test_workload4_pythia_headline():
+def test_pythia_1_4b_headline():
     """N=8, c=64, d=1,414,647,808 (the headline size), kappa_max = 1e3 design,
     bench launch sequence; 65,536 sampled positions x 64 chunks x 8 workers."""
     torch, dev = torch_dev()
-    wl = synth.workload(4)
+    wl = synth.workload("pythia-1.4b")
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
     U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(wl.c)), 0.3, 1e3, 20, order="projected")
     kappa = OP.max_kappa_M(U)
@@ -176,16 +176,16 @@ def test_workload4_pythia_headline():
     run_stepwise(plan, wl.d, grads, work, ws, out)
     torch.cuda.synchronize()
     p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
-    check_sampled("workload4", wl, U, R, grads, out, sample_positions(p, 65536, 4), kappa)
+    check_sampled("pythia-1.4b", wl, U, R, grads, out, sample_positions(p, 65536, 4), kappa)
 
 
-def test_workload5_heavy_tail_n16_c128():
+def test_heavy_tail_n16_c128():
     """N=16, c=128, d=4e8 with 1% x100 outliers.  A well-conditioned plan
     (orthogonal U_k, least-squares R_i) is gated; the O(eps=1e-2) plan of the
     workload (r_star = 7, kappa(A_l) ~ 1e20: singular even in fp64) is only
     reported, against Prop. 1's closed-form output, which needs no inverse."""
     torch, dev = torch_dev()
-    wl = synth.workload(5)
+    wl = synth.workload("heavytail-n16-c128")
     grads = device_grads(wl, torch, dev)
     p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
     pos = sample_positions(p, 8192, 5)
@@ -196,7 +196,7 @@ def test_workload5_heavy_tail_n16_c128():
     work, ws, out = C.allocate(plan, wl.d, dev)
     run_stepwise(plan, wl.d, grads, work, ws, out)
     torch.cuda.synchronize()
-    check_sampled("workload5 orthogonal plan", wl, U, R, grads, out, pos, kappa)
+    check_sampled("heavytail-n16-c128 orthogonal plan", wl, U, R, grads, out, pos, kappa)
     plan.close()
     # reported: the O(eps) plan of the workload
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
@@ -214,7 +214,7 @@ def test_workload5_heavy_tail_n16_c128():
     dev_orc = max(per_worker_rel([r[valid] for r in ref], [x[valid] for x in closed]))
     S = sum(g[valid] for g in G)
     err_closed = max(per_worker_rel([x[valid] for x in closed], [S] * wl.N))
-    print(f"workload5 O(eps=1e-2): max|U|={np.abs(U).max():.3g}; deviation from the Prop. 1 "
+    print(f"heavytail-n16-c128 O(eps=1e-2): max|U|={np.abs(U).max():.3g}; deviation from the Prop. 1 "
           f"closed form: gpu {dev_gpu:.3g}, fp64 oracle {dev_orc:.3g}; closed-form error vs the "
           f"exact sum {err_closed:.4g}", flush=True)
     assert err_closed < 0.1                            # the plan itself is accurate (Prop. 2)

@@ -25,8 +25,8 @@ def test_splitmix64_matches_published_sequence():
 def test_numpy_and_torch_paths_give_identical_bits():
     torch = pytest.importorskip("torch")
     rng = np.random.default_rng(0)
-    for cfg in (1, 3, 4, 5):
-        wl = synth.workload(cfg)
+    for name in ("tiny-n4-c4", "gpt2-small", "pythia-1.4b", "heavytail-n16-c128"):
+        wl = synth.workload(name)
         idx = np.unique(np.concatenate([rng.integers(0, wl.d, 20000), [0, wl.d - 1, wl.d, wl.d + 5]]))
         for w in (0, wl.N - 1):
             a = wl.values_np(w, idx)
@@ -43,7 +43,7 @@ def test_numpy_and_torch_paths_give_identical_bits():
 
 def test_fill_matches_pointwise_values():
     torch = pytest.importorskip("torch")
-    wl = synth.workload(3)
+    wl = synth.workload("gpt2-small")
     out = torch.empty(10007, dtype=torch.float32)
     wl.fill_torch(out, 2, start=wl.d - 5000, chunk=4096)
     ref = wl.values_np(2, np.arange(wl.d - 5000, wl.d - 5000 + 10007))
@@ -62,7 +62,7 @@ def test_irwin_hall_normal_moments():
 
 
 def test_workers_are_independent_streams():
-    wl = synth.workload(2)
+    wl = synth.workload("iid-n8-c16-16m")
     idx = np.arange(200_000)
     a = wl.values_np(0, idx).astype(np.float64)
     b = wl.values_np(1, idx).astype(np.float64)
@@ -71,7 +71,7 @@ def test_workers_are_independent_streams():
 
 
 def test_outliers_are_one_percent_at_100x():
-    wl = synth.workload(5)
+    wl = synth.workload("heavytail-n16-c128")
     idx = np.arange(400_000)
     key = wl.worker_key(3)
     hit = synth.uniform32_np(key, idx, 6) < wl.outlier_threshold
@@ -87,11 +87,11 @@ def test_model_shapes():
     assert len(g) == 148 and sum(g) == 124_439_808
     p = synth.pythia_1_4b_tensor_sizes()
     assert len(p) == 292 and sum(p) == 1_414_647_808
-    assert synth.workload(4).d == 1_414_647_808 and synth.workload(3).d == 124_439_808
+    assert synth.workload("pythia-1.4b").d == 1_414_647_808 and synth.workload("gpt2-small").d == 124_439_808
 
 
 def test_per_tensor_scales_are_lognormal_and_shared():
-    wl = synth.workload(4)
+    wl = synth.workload("pythia-1.4b")
     s = wl.tensor_scales().astype(np.float64)
     z = np.log(s)
     assert len(s) == 292
@@ -119,7 +119,7 @@ def test_ddp_buckets_cover_the_gradient():
         if ln > synth.DDP_BUCKET_FLOATS:                   # only a single oversize tensor
             assert ln in sizes
     assert pos == d
-    assert synth.workload(3).buckets == b
+    assert synth.workload("gpt2-small").buckets == b
 
 
 def test_base_matrix_is_seeded():
