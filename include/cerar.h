@@ -22,9 +22,14 @@
  *  - Pointers named "device" are HIP device memory of the current device,
  *    owned by the caller; the library never frees caller memory.
  *  - Calls taking a stream only validate and enqueue work on that stream
- *    (NULL = the legacy default stream); they never synchronise.  Work
- *    enqueued by calls that share buffers must be ordered by the caller
- *    (one stream does that).
+ *    (NULL = the legacy default stream); they never synchronise, with one
+ *    exception: the first such call for a plan on a device uploads the
+ *    plan's fp32 coefficients and tables to that device (hipMalloc and a
+ *    synchronous hipMemcpy, once per plan and device).  After it, the calls
+ *    issue kernel launches only (no allocation, copy or memset), so they can
+ *    be recorded into a HIP graph by stream capture.  Work enqueued by calls
+ *    that share buffers must be ordered by the caller (one stream does
+ *    that).
  *  - All floating point on the device is IEEE fp32; plan construction is
  *    host fp64.
  */

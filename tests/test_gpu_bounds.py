@@ -52,6 +52,7 @@ CASES = [
     (2, 128, 128 * 640, 0, 0, 0),        # c = 128 interior blocks: the wide MFMA kernels
     (3, 128, 128 * 640 - 17, 0, 4, 4),   # ... plus a ragged tail on the generic ones
     (16, 32, 32 * 96 + 5, 4, 8, 12),
+    (64, 128, 128 * 640 - 3, 0, 4, 4),   # largest N and c
 ]
 
 

@@ -1,0 +1,124 @@
+"""The enqueueing calls can be recorded into a HIP graph.
+
+After one eager call on the device (the call that uploads the plan's fp32
+coefficients and tables), cerar_ring_simulate, its bucketed form and the
+fused variant issue only kernel launches on the given stream, so
+torch.cuda.graph can capture them.  Every replay runs on fresh inputs copied
+into the captured buffers, with an eager call of the same entry point on
+separate buffers and a synchronisation between replays, and must give
+exactly the eager result; the first replay is also checked against the
+oracle."""
+
+import numpy as np
+import pytest
+
+from paper_2609_23898_amd import cerar as C
+
+from gpu_util import buffers, host_grads, max_rel_l2, oracle_allreduce, orthogonal_plan, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+REPLAYS = 3
+
+
+def _check_replays(call, make_bufs, inputs, d, oracle_check):
+    """call(bufs) enqueues one all-reduce on the current stream; make_bufs()
+    gives fresh buffers (grads first, out last, both (N, >= d)); inputs[r]
+    is the (N, d) input of replay r; oracle_check(out, g) checks one
+    result against the oracle."""
+    torch, _ = torch_dev()
+
+    def load(bufs, g):
+        bufs[0][:, :d].copy_(torch.from_numpy(g).to(bufs[0].device))
+        bufs[-1].fill_(float("nan"))
+
+    cap, ref = make_bufs(), make_bufs()
+    load(cap, inputs[0])
+    call(cap)                                   # eager: uploads the plan to this device
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        call(cap)
+    torch.cuda.synchronize()
+    for r, g in enumerate(inputs):
+        load(cap, g)
+        graph.replay()
+        torch.cuda.synchronize()
+        load(ref, g)
+        call(ref)                               # the eager result for the same inputs
+        torch.cuda.synchronize()
+        got = cap[-1][:, :d].cpu().numpy()
+        assert np.all(np.isfinite(got)), f"replay {r}"
+        np.testing.assert_array_equal(got, ref[-1][:, :d].cpu().numpy(), err_msg=f"replay {r}")
+        if r == 0:
+            oracle_check(got.astype(np.float64), g)
+    del graph
+
+
+def test_ring_simulate_replays_from_a_graph():
+    torch, dev = torch_dev()
+    N, c, d = 8, 32, 32 * 2048 + 7
+    U, R = orthogonal_plan(N, c, seed=31)
+    plan = C.Plan.explicit(U, R)
+
+    def make_bufs():
+        return (torch.zeros((N, d), dtype=torch.float32, device=dev),) + tuple(buffers(plan, d))
+
+    def call(b):
+        C.ring_simulate(plan, d, b[0], b[1], b[2], b[3])
+
+    def oracle_check(out, g):
+        assert max_rel_l2(out, oracle_allreduce(g, U, R)) <= 1e-4
+
+    inputs = [host_grads(N, d, seed=310 + r) for r in range(REPLAYS)]
+    _check_replays(call, make_bufs, inputs, d, oracle_check)
+
+
+def test_bucketed_replays_from_a_graph():
+    torch, dev = torch_dev()
+    N, c = 4, 16
+    lens = [16 * 32 * 9, 16 * 32 * 3 - 4, 16 * 32 * 17 - 12, 4]      # 16-byte aligned: the batched kernels
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).tolist()
+    buckets = [(int(o), int(n)) for o, n in zip(offs, lens)]
+    d = buckets[-1][0] + buckets[-1][1]
+    U, R = orthogonal_plan(N, c, seed=32)
+    plan = C.Plan.explicit(U, R)
+    work_floats, ws_bytes = plan.bucketed_sizes(lens)
+
+    def make_bufs():
+        return (torch.zeros((N, d), dtype=torch.float32, device=dev),
+                torch.empty((N, work_floats), dtype=torch.float32, device=dev),
+                torch.zeros(ws_bytes, dtype=torch.uint8, device=dev),
+                torch.empty((N, d), dtype=torch.float32, device=dev))
+
+    def call(b):
+        C.ring_simulate_bucketed(plan, buckets, b[0], b[1], b[2], b[3])
+
+    def oracle_check(out, g):
+        for off, ln in buckets:                 # each bucket is its own all-reduce
+            want = oracle_allreduce(g[:, off:off + ln], U, R)
+            assert max_rel_l2(out[:, off:off + ln], want) <= 1e-4, (off, ln)
+
+    inputs = [host_grads(N, d, seed=320 + r) for r in range(REPLAYS)]
+    _check_replays(call, make_bufs, inputs, d, oracle_check)
+
+
+def test_fused_variant_replays_from_a_graph():
+    torch, dev = torch_dev()
+    N, c, d = 8, 64, 64 * 300 + 9
+    ld = (d + 3) // 4 * 4                       # the fused variant needs 16-byte aligned rows
+    U, R = orthogonal_plan(N, c, seed=33)
+    plan = C.Plan.explicit(U, R)
+
+    def make_bufs():
+        return (torch.zeros((N, ld), dtype=torch.float32, device=dev),
+                torch.empty((N, ld), dtype=torch.float32, device=dev))
+
+    def call(b):
+        C.ring_simulate_fused(plan, d, b[0], b[1])
+
+    def oracle_check(out, g):
+        assert max_rel_l2(out, oracle_allreduce(g, U, R)) <= 1e-4
+
+    inputs = [host_grads(N, d, seed=330 + r) for r in range(REPLAYS)]
+    _check_replays(call, make_bufs, inputs, d, oracle_check)

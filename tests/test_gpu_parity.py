@@ -174,6 +174,7 @@ EDGE = [
     ("N2-c128", 2, 128, 128 * 70 + 5),     # largest c, smallest N
     ("N64-c64-exact", 64, 64, 64 * 80),    # largest N
     ("N64-c65", 64, 65, 65 * 64 + 1),
+    ("N64-c128", 64, 128, 128 * 640 - 3),  # largest N and c: L = 190, the 48-K-step wide decode
     ("p-63", 4, 16, 16 * 63),              # one partial 64-position block
     ("p-64", 4, 16, 16 * 64),              # exactly one block
     ("p-65", 4, 16, 16 * 65),
