@@ -49,7 +49,7 @@ typedef struct ihipStream_t *cerar_stream;
 typedef enum {
     CERAR_OK = 0,
     CERAR_E_INVAL = -1,    /* an argument is out of range or NULL */
-    CERAR_E_NOMEM = -2,    /* host or device allocation failed */
+    CERAR_E_NOMEM = -2,    /* a host or device allocation failed, or another host resource (a thread) */
     CERAR_E_SINGULAR = -3, /* some window A_l of the construction is exactly singular */
     CERAR_E_NOCONV = -4,   /* an iterative host routine did not converge */
     CERAR_E_DEVICE = -5,   /* a HIP call failed; the HIP error text is in cerar_last_error() */

@@ -1,8 +1,10 @@
 // Internal structures shared by the host plan code and the HIP launchers.
 #pragma once
 
+#include <exception>
 #include <map>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -73,8 +75,25 @@ struct cerar_plan {
 
 namespace cerar {
 // Thread-local error text; returns `status` for convenient `return fail(...)`.
-int fail(int status, const char *fmt, ...);
-void clear_error();
+int fail(int status, const char *fmt, ...) noexcept;
+void clear_error() noexcept;
+
+// Runs the body of a C entry point and turns a C++ exception into a status,
+// so that none unwinds through the C ABI: a failed host allocation, or a
+// host resource that could not be had, is CERAR_E_NOMEM.
+template <class F>
+int guarded(F &&body) noexcept {
+    try {
+        return body();
+    } catch (const std::bad_alloc &) {
+        return fail(CERAR_E_NOMEM, "out of host memory");
+    } catch (const std::exception &e) {
+        return fail(CERAR_E_NOMEM, "host resources exhausted: %s", e.what());
+    } catch (...) {
+        return fail(CERAR_E_NOMEM, "unexpected host exception");
+    }
+}
+
 // Fills MT/KSe/KSd and the fp32 fragment arrays from U and R.
 void build_fragments(cerar_plan *plan);
 // Releases device copies (called by cerar_plan_destroy; defined with the kernels).

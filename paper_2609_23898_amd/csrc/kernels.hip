@@ -1419,7 +1419,8 @@ int device_copy(const cerar_plan *plan, const DeviceCopy **out) {
         *out = &it->second;
         return CERAR_OK;
     }
-    DeviceCopy dc;
+    // The map entry comes first: once device memory is held, nothing here throws.
+    DeviceCopy &dc = plan->dev[dev];
     int st = upload(&dc.enc_frag, plan->enc_frag.data(), plan->enc_frag.size());
     if (!st) st = upload(&dc.dec_frag, plan->dec_frag.data(), plan->dec_frag.size());
     if (!st) st = upload(&dc.ycols, plan->tab.ycols.data(), plan->tab.ycols.size());
@@ -1429,9 +1430,10 @@ int device_copy(const cerar_plan *plan, const DeviceCopy **out) {
         (void)hipFree(dc.dec_frag);
         (void)hipFree(dc.ycols);
         (void)hipFree(dc.rounds);
+        plan->dev.erase(dev);
         return st;
     }
-    *out = &(plan->dev[dev] = dc);
+    *out = &dc;
     return CERAR_OK;
 }
 
@@ -1869,9 +1871,8 @@ void release_device(cerar_plan *plan) {
 
 using namespace cerar;
 
-extern "C" int cerar_encode_round(const cerar_plan *plan, int step, size_t d, const float *grads,
-                                  size_t ld_grads, float *work, size_t ld_work, void *ws, cerar_stream stream) {
-    clear_error();
+static int encode_round_impl(const cerar_plan *plan, int step, size_t d, const float *grads,
+                             size_t ld_grads, float *work, size_t ld_work, void *ws, cerar_stream stream) {
     Geometry g;
     int st = check_common(plan, d, work, ld_work, ws, g);
     if (st) return st;
@@ -1900,9 +1901,14 @@ extern "C" int cerar_encode_round(const cerar_plan *plan, int step, size_t d, co
     return CERAR_OK;
 }
 
-extern "C" int cerar_decode(const cerar_plan *plan, size_t d, const float *work, size_t ld_work, const void *ws,
-                            float *out, size_t ld_out, cerar_stream stream) {
+extern "C" int cerar_encode_round(const cerar_plan *plan, int step, size_t d, const float *grads,
+                                  size_t ld_grads, float *work, size_t ld_work, void *ws, cerar_stream stream) {
     clear_error();
+    return guarded([&] { return encode_round_impl(plan, step, d, grads, ld_grads, work, ld_work, ws, stream); });
+}
+
+static int decode_impl(const cerar_plan *plan, size_t d, const float *work, size_t ld_work, const void *ws,
+                       float *out, size_t ld_out, cerar_stream stream) {
     Geometry g;
     int st = check_common(plan, d, work, ld_work, ws, g);
     if (st) return st;
@@ -1922,10 +1928,15 @@ extern "C" int cerar_decode(const cerar_plan *plan, size_t d, const float *work,
     return enqueue_decode(plan, dc, g, d, work, ld_work, ws, out, ld_out, reinterpret_cast<hipStream_t>(stream));
 }
 
-extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
-                                   float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
-                                   cerar_stream stream) {
+extern "C" int cerar_decode(const cerar_plan *plan, size_t d, const float *work, size_t ld_work, const void *ws,
+                            float *out, size_t ld_out, cerar_stream stream) {
     clear_error();
+    return guarded([&] { return decode_impl(plan, d, work, ld_work, ws, out, ld_out, stream); });
+}
+
+static int ring_simulate_impl(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                              float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
+                              cerar_stream stream) {
     Geometry g;
     int st = check_common(plan, d, work, ld_work, ws, g);
     if (st) return st;
@@ -1944,6 +1955,15 @@ extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float
     std::lock_guard<std::mutex> lk(g_cursor_mu);
     g_cursor[ws] = Cursor{plan, plan->L + 1, d};
     return CERAR_OK;
+}
+
+extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                   float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
+                                   cerar_stream stream) {
+    clear_error();
+    return guarded([&] {
+        return ring_simulate_impl(plan, d, grads, ld_grads, work, ld_work, ws, out, ld_out, stream);
+    });
 }
 
 namespace {
@@ -2000,9 +2020,8 @@ int launch_fused_lanes_c(const FusedParams &a, const BlockSplit &bs, hipStream_t
 }
 }  // namespace
 
-extern "C" int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
-                                         float *out, size_t ld_out, cerar_stream stream) {
-    clear_error();
+static int ring_simulate_fused_impl(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                    float *out, size_t ld_out, cerar_stream stream) {
     if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
     if (d == 0 || !grads || !out) return fail(CERAR_E_INVAL, "d > 0 and non-NULL buffers required");
     const int N = plan->N, c = plan->c;
@@ -2056,6 +2075,12 @@ extern "C" int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const
     }
     HIP_TRY(hipGetLastError(), "launch fused");
     return CERAR_OK;
+}
+
+extern "C" int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                         float *out, size_t ld_out, cerar_stream stream) {
+    clear_error();
+    return guarded([&] { return ring_simulate_fused_impl(plan, d, grads, ld_grads, out, ld_out, stream); });
 }
 
 extern "C" int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_grads, const float *out,
@@ -2249,19 +2274,23 @@ int enqueue_decode_buckets(const cerar_plan *plan, const DeviceCopy *dc, const s
 
 }  // namespace
 
-extern "C" int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len, int nbuckets,
-                                              size_t *work_floats, size_t *ws_bytes) {
-    clear_error();
+static int bucketed_workspace_bytes_impl(const cerar_plan *plan, const size_t *bucket_len, int nbuckets,
+                                         size_t *work_floats, size_t *ws_bytes) {
     if (!work_floats || !ws_bytes) return fail(CERAR_E_INVAL, "NULL output");
     std::vector<BucketLayout> lay;
     return bucket_layout(plan, nbuckets, bucket_len, lay, *work_floats, *ws_bytes);
 }
 
-extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets, const size_t *bucket_off,
-                                            const size_t *bucket_len, const float *grads, size_t ld_grads,
-                                            float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
-                                            cerar_stream stream) {
+extern "C" int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len, int nbuckets,
+                                              size_t *work_floats, size_t *ws_bytes) {
     clear_error();
+    return guarded([&] { return bucketed_workspace_bytes_impl(plan, bucket_len, nbuckets, work_floats, ws_bytes); });
+}
+
+static int ring_simulate_bucketed_impl(const cerar_plan *plan, int nbuckets, const size_t *bucket_off,
+                                       const size_t *bucket_len, const float *grads, size_t ld_grads,
+                                       float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
+                                       cerar_stream stream) {
     std::vector<BucketLayout> lay;
     size_t work_floats, ws_bytes;
     int st = bucket_layout(plan, nbuckets, bucket_len, lay, work_floats, ws_bytes);
@@ -2357,4 +2386,15 @@ extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets
         st = enqueue_decode(plan, dc, geo[b], bucket_len[b], work + lay[b].work_off, ld_work,
                             (char *)ws + lay[b].ws_off, out + bucket_off[b], ld_out, s);
     return st;
+}
+
+extern "C" int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets, const size_t *bucket_off,
+                                            const size_t *bucket_len, const float *grads, size_t ld_grads,
+                                            float *work, size_t ld_work, void *ws, float *out, size_t ld_out,
+                                            cerar_stream stream) {
+    clear_error();
+    return guarded([&] {
+        return ring_simulate_bucketed_impl(plan, nbuckets, bucket_off, bucket_len, grads, ld_grads, work, ld_work,
+                                           ws, out, ld_out, stream);
+    });
 }

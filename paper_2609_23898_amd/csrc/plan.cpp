@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstring>
 #include <limits>
+#include <memory>
 #include <set>
 #include <thread>
 
@@ -14,19 +15,18 @@
 
 namespace cerar {
 
-static thread_local std::string g_last_error;
+// A fixed buffer, so that recording an error never allocates or throws.
+static thread_local char g_last_error[512];
 
-int fail(int status, const char *fmt, ...) {
-    char buf[512];
+int fail(int status, const char *fmt, ...) noexcept {
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
     va_end(ap);
-    g_last_error = buf;
     return status;
 }
 
-void clear_error() { g_last_error.clear(); }
+void clear_error() noexcept { g_last_error[0] = 0; }
 
 namespace {
 
@@ -62,20 +62,37 @@ std::vector<double> chebyshev_nodes(int c) {
     return x;
 }
 
-// Runs f(k) for k in [0, n) on up to hardware_concurrency threads.
+// Runs f(k) for k in [0, n) on up to hardware_concurrency threads, thread t
+// taking k = t, t + nt, ...  The share of a thread that cannot be started runs
+// on the calling thread.  An exception thrown by f on any thread is rethrown
+// here, after every thread has been joined.
 template <class F>
 void parallel_for(int n, F f) {
-    int nt = (int)std::min<unsigned>(std::max(1u, std::thread::hardware_concurrency()), (unsigned)n);
+    const int nt = (int)std::min<unsigned>(std::max(1u, std::thread::hardware_concurrency()), (unsigned)std::max(n, 0));
     if (nt <= 1) {
         for (int k = 0; k < n; ++k) f(k);
         return;
     }
-    std::vector<std::thread> th;
-    for (int t = 0; t < nt; ++t)
-        th.emplace_back([&, t] {
+    std::exception_ptr err;
+    std::mutex mu;
+    auto share = [&](int t) {
+        try {
             for (int k = t; k < n; k += nt) f(k);
-        });
+        } catch (...) {
+            std::lock_guard<std::mutex> g(mu);
+            if (!err) err = std::current_exception();
+        }
+    };
+    std::vector<std::thread> th;
+    th.reserve(nt);
+    int started = 0;
+    try {
+        for (; started < nt; ++started) th.emplace_back(share, started);
+    } catch (...) {
+    }
+    for (int t = started; t < nt; ++t) share(t);
     for (auto &x : th) x.join();
+    if (err) std::rethrow_exception(err);
 }
 
 // ---- multiplicative perturbation construction (eqs. (8)-(11)) -------------
@@ -497,8 +514,7 @@ static int finish_plan(cerar_plan *p, cerar_construction kind, double param, cer
     return CERAR_OK;
 }
 
-extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
-    clear_error();
+static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
     if (!out) return fail(CERAR_E_INVAL, "out is NULL");
     *out = nullptr;
     int st = validate(desc);
@@ -518,8 +534,8 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
     } else {
         for (int j = 0; j < c; ++j) H[(size_t)j * c + j] = nodes[j];
     }
-    cerar_plan *p = new (std::nothrow) cerar_plan();
-    if (!p) return fail(CERAR_E_NOMEM, "out of host memory");
+    std::unique_ptr<cerar_plan> holder(new cerar_plan());   // freed on every failure, thrown or returned
+    cerar_plan *p = holder.get();
     p->N = N;
     p->c = c;
     p->L = c + N - 2;
@@ -542,10 +558,8 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
         const double eps = desc->kind == CERAR_O_EPS ? desc->param : (desc->eps0 > 0 ? desc->eps0 : 0.3);
         if (desc->kind == CERAR_O_EPS && eps > 0) {
             std::vector<double> s = la::singular_values(H.data(), c, c);
-            if (eps * s.front() >= 1.0) {
-                delete p;
+            if (eps * s.front() >= 1.0)
                 return fail(CERAR_E_INVAL, "eps ||H||_2 = %g must be < 1 (Sec. II-C)", eps * s.front());
-            }
         }
         const int tries = desc->base ? 1 : 8;
         for (int t = 0; t < tries; ++t) {
@@ -605,8 +619,37 @@ extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **
         }
     }
     if (result == CERAR_OK) result = finish_plan(p, desc->kind, desc->param, out);
-    if (result != CERAR_OK) delete p;
+    if (result == CERAR_OK) holder.release();
     return result;
+}
+
+static int create_explicit(int N, int c, const double *U, const double *R, cerar_plan **out) {
+    if (!out) return fail(CERAR_E_INVAL, "out is NULL");
+    *out = nullptr;
+    if (!U || !R) return fail(CERAR_E_INVAL, "U and R must be non-NULL");
+    if (N < 2 || N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [2, %d]", N, kMaxN);
+    if (c < N || c > kMaxC) return fail(CERAR_E_INVAL, "c=%d outside [N=%d, %d]", c, N, kMaxC);
+    std::unique_ptr<cerar_plan> holder(new cerar_plan());
+    cerar_plan *p = holder.get();
+    p->N = N;
+    p->c = c;
+    p->L = c + N - 2;
+    p->U.assign(U, U + (size_t)N * c * c);
+    p->R.assign(R, R + (size_t)N * (p->L + 1) * c);
+    p->info.phi_initial = kNaN;
+    p->info.proj_a0 = p->info.proj_b0 = kNaN;
+    p->info.gamma = kNaN;
+    p->info.h_choice = -1;
+    int result = finish_plan(p, CERAR_EXPLICIT, kNaN, out);
+    if (result == CERAR_OK) holder.release();
+    return result;
+}
+
+extern "C" int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
+    clear_error();
+    const int st = guarded([&] { return create_desc(desc, out); });
+    if (st != CERAR_OK && out) *out = nullptr;
+    return st;
 }
 
 extern "C" int cerar_plan_create(int N, int c, cerar_construction kind, double param, uint64_t seed,
@@ -623,25 +666,9 @@ extern "C" int cerar_plan_create(int N, int c, cerar_construction kind, double p
 
 extern "C" int cerar_plan_create_explicit(int N, int c, const double *U, const double *R, cerar_plan **out) {
     clear_error();
-    if (!out) return fail(CERAR_E_INVAL, "out is NULL");
-    *out = nullptr;
-    if (!U || !R) return fail(CERAR_E_INVAL, "U and R must be non-NULL");
-    if (N < 2 || N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [2, %d]", N, kMaxN);
-    if (c < N || c > kMaxC) return fail(CERAR_E_INVAL, "c=%d outside [N=%d, %d]", c, N, kMaxC);
-    cerar_plan *p = new (std::nothrow) cerar_plan();
-    if (!p) return fail(CERAR_E_NOMEM, "out of host memory");
-    p->N = N;
-    p->c = c;
-    p->L = c + N - 2;
-    p->U.assign(U, U + (size_t)N * c * c);
-    p->R.assign(R, R + (size_t)N * (p->L + 1) * c);
-    p->info.phi_initial = kNaN;
-    p->info.proj_a0 = p->info.proj_b0 = kNaN;
-    p->info.gamma = kNaN;
-    p->info.h_choice = -1;
-    int result = finish_plan(p, CERAR_EXPLICIT, kNaN, out);
-    if (result != CERAR_OK) delete p;
-    return result;
+    const int st = guarded([&] { return create_explicit(N, c, U, R, out); });
+    if (st != CERAR_OK && out) *out = nullptr;
+    return st;
 }
 
 extern "C" void cerar_plan_destroy(cerar_plan *plan) {
@@ -696,4 +723,4 @@ extern "C" int cerar_slot_map(const cerar_plan *plan, int step, int *slots) {
     return CERAR_OK;
 }
 
-extern "C" const char *cerar_last_error(void) { return cerar::g_last_error.c_str(); }
+extern "C" const char *cerar_last_error(void) { return cerar::g_last_error; }
