@@ -1,0 +1,120 @@
+"""Host logic of bench.py, on the CPU: the algorithmic byte count of a step,
+the launch families, the rocprofv3 summaries (on small synthetic CSV files
+in rocprofv3's column layout) and the refusal of more than one GPU."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+import bench
+from conftest import ROOT
+from paper_2609_23898_amd import cerar as C
+
+
+@pytest.mark.parametrize("N,c", [(2, 2), (2, 5), (4, 4), (4, 9), (8, 16), (8, 64), (16, 128), (64, 128)])
+def test_step_bytes_match_the_stream_count(N, c):
+    """Encode: c chunks read, c written, plus the message-1 copy.  Rounds
+    1..N-1: receive + delta read, message written (3 streams); rounds N..c-1:
+    receive, two deltas read, message written (4); rounds c..L-1: receive and
+    one delta read, message written (3); round L only relabels.  Decode: L+1
+    observations read, c outputs written.  Summed: (8c + 3N - 9) p floats."""
+    p = 96
+    b = C.phase_bytes_per_worker(N, c, p)
+    L = c + N - 2
+    assert sorted(b["rounds"]) == list(range(1, L + 1))
+    assert b["rounds"][L] == 0
+    total = b["encode"] + sum(b["rounds"].values()) + b["decode"]
+    assert total == (8 * c + 3 * N - 9) * p * 4
+
+
+def test_headline_step_bytes_and_launch_families():
+    """N=8, c=64, d=1,414,647,808: p = 22,103,872 and 372,759,697,408 bytes
+    per step; 7 rounds of K2, 56 of K3 with two deltas, 6 with one."""
+    N, c, d = 8, 64, 1_414_647_808
+    p = -(-d // c)
+    assert p == 22_103_872 and p % 32 == 0
+    b = C.phase_bytes_per_worker(N, c, p)
+    assert N * (b["encode"] + sum(b["rounds"].values()) + b["decode"]) == 372_759_697_408
+    L = c + N - 2
+    fams = [bench.family_of(k, N, c, L) for k in range(1, L + 1)]
+    assert fams.count("k_round<0> (K2: recv + delta)") == N - 1 == 7
+    assert fams.count("k_round<1> (K3: recv - delta + delta)") == c - N == 56
+    assert fams.count("k_round<2> (K3: recv - delta)") == N - 2 == 6
+    assert fams[-1] is None
+    per_launch = bench._step_bytes_cfg4()
+    assert per_launch["k_round<1> (K3: recv - delta + delta)"] == N * 4 * p * 4
+    assert per_launch["k_encode (K1)"] == N * (2 * c + 1) * p * 4
+
+
+def test_kernel_names_map_to_families():
+    assert bench.family_of_name("k_encode_dbuf<16, 4>") == "k_encode (K1)"
+    assert bench.family_of_name("k_round<1, true>") == "k_round<1> (K3: recv - delta + delta)"
+    assert bench.family_of_name("k_round<0, false>") == "k_round<0> (K2: recv + delta)"
+    assert bench.family_of_name("k_decode_wide<48, 8>") == "k_decode (K4)"
+    assert bench.family_of_name("k_copy4") == "k_copy4 (copy reference)"
+    assert bench.family_of_name("k_fused_lanes<4, 8, true>") is None
+    assert bench.family_of_name("k_norms") is None
+
+
+def _write_csv(path, header, rows):
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as f:
+        f.write(",".join(header) + "\n")
+        for r in rows:
+            f.write(",".join(str(x) for x in r) + "\n")
+
+
+def test_counter_summary_is_scaled_by_the_copy_kernel(tmp_path):
+    """FETCH_SIZE reads half the copy kernel's bytes (as on gfx950) and
+    WRITE_SIZE all of them: both are divided by their copy-kernel factor."""
+    copy_floats = 1 << 20
+    copy_kib = copy_floats * 4 / 1024
+    enc = "void cerar::(anonymous namespace)::k_encode_dbuf<16, 4>(cerar::(anonymous namespace)::EncParams)"
+    hdr = ["Kernel_Name", "Counter_Name", "Counter_Value"]
+    _write_csv(str(tmp_path / "fetch" / "host" / "pmc_counter_collection.csv"), hdr,
+               [["k_copy4", "FETCH_SIZE", copy_kib * 0.5], [f'"{enc}"', "FETCH_SIZE", 1000.0],
+                [f'"{enc}"', "FETCH_SIZE", 1200.0]])
+    _write_csv(str(tmp_path / "write" / "host" / "pmc_counter_collection.csv"), hdr,
+               [["k_copy4", "WRITE_SIZE", copy_kib], [f'"{enc}"', "WRITE_SIZE", 3000.0],
+                [f'"{enc}"', "WRITE_SIZE", 3000.0]])
+    out = tmp_path / "summary.txt"
+    bench.summarize_pmc(str(tmp_path / "fetch"), str(tmp_path / "write"), str(out), copy_floats=copy_floats)
+    text = out.read_text()
+    assert "fetch_scale: 0.50000" in text and "write_scale: 1.00000" in text
+    expect = (1100.0 / 0.5 + 3000.0) * 1024
+    assert f"traffic_bytes_per_launch[k_encode (K1)]: {expect:.0f}" in text
+    assert f"kernel_source_sha256: {bench.kernel_source_hash()}" in text
+
+
+def test_trace_summary_compares_trace_and_event_averages(tmp_path):
+    hdr = ["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage"]
+    _write_csv(str(tmp_path / "trace" / "host" / "trace_kernel_stats.csv"), hdr, [
+        ['"void cerar::(anonymous namespace)::k_round<1, true>(cerar::(anonymous namespace)::RoundParams)"',
+         10, 4_400_000, 440_000, 60.0],
+        ['"void cerar::(anonymous namespace)::k_round<1, false>(cerar::(anonymous namespace)::RoundParams)"',
+         10, 4_600_000, 460_000, 30.0],
+        ['"void at::native::elementwise_kernel<128, 4>(int)"', 5, 500_000, 100_000, 10.0]])
+    line = {"ms_per_step": 65.0, "value": 5700.0, "config": {"pct_hbm_peak": 71.3},
+            "roofline": {"kernel": "k_round<1> (K3: recv - delta + delta)", "achieved": 6300.0},
+            "kernels": {"k_round<1> (K3: recv - delta + delta)": {"avg_ms": 0.459}}}
+    log = tmp_path / "bench.log"
+    log.write_text("some text\n" + json.dumps(line) + "\n")
+    out = tmp_path / "trace.txt"
+    bench.summarize_trace(str(tmp_path / "trace"), str(log), str(out))
+    rows = [r for r in out.read_text().splitlines() if r.startswith("k_round<1> (K3")]
+    assert len(rows) == 1
+    trace_avg, event_avg, ratio = (float(x) for x in rows[0].split()[-3:])
+    assert trace_avg == pytest.approx(0.45) and event_avg == pytest.approx(0.459)
+    assert ratio == pytest.approx(0.459 / 0.45, abs=1e-3)
+    assert "other kernels (torch input generation, untimed)" in out.read_text()
+
+
+def test_more_than_one_gpu_is_refused():
+    run = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=300)
+    assert run.returncode == 2
+    assert "--gpus 2 is not supported" in run.stderr
+    assert run.stdout.strip() == ""
