@@ -1484,6 +1484,12 @@ SlotBase slot_base(const cerar_plan *plan, const Geometry &g, float *work, size_
 // one sweeps: about 4 passes of its 4 waves, so that the workgroups resident
 // at one time cover one compact window of positions in every row (measured
 // faster on MI355X than interleaving the passes across the grid).
+// One dispatch holds at most 2^31 - 1 workgroups along x and fewer than 2^32
+// work-items along x (the packet's grid size is a 32-bit work-item count).
+bool fits_dispatch(uint64_t wgs, unsigned threads) {
+    return wgs >= 1 && wgs <= 0x7fffffffu && wgs * threads <= 0xffffffffu;
+}
+
 void wg_for(size_t nblk, int &wg_per_worker, size_t &blk_per_wg) {
     size_t w = (nblk + 4 * kWaves - 1) / (4 * kWaves);
     if (w < 1) w = 1;
@@ -1753,6 +1759,8 @@ int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &
     a.sb = slot_base(plan, g, work, ld_work, ws);
     a.ops = dc->rounds + (size_t)k * N;
     a.wg_per_worker = (int)round_wgs(g.p, g.vec);
+    if (!fits_dispatch((uint64_t)N * a.wg_per_worker, kRoundThreads))
+        return fail(CERAR_E_INVAL, "p=%zu is too long for one round launch over N=%d workers", g.p, N);
     const dim3 grid((unsigned)(N * a.wg_per_worker));
     (void)c;
     const int mode = round_mode(plan, k);
@@ -2109,7 +2117,8 @@ extern "C" int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stre
     if (n % 4 == 0 && aligned16(dst) && aligned16(src)) {
         const size_t n4 = n / 4;
         const size_t blocks = (n4 + kCopyThreads - 1) / kCopyThreads;
-        if (blocks > 0x7fffffffu) return fail(CERAR_E_INVAL, "copy of %zu floats is too large for one launch", n);
+        if (!fits_dispatch(blocks, kCopyThreads))
+            return fail(CERAR_E_INVAL, "copy of %zu floats is too large for one launch", n);
         hipLaunchKernelGGL(k_copy4, dim3((unsigned)blocks), dim3(kCopyThreads), 0, s, dst, src, n4);
     } else {
         size_t blocks = std::max<size_t>(1, std::min<size_t>((n + kThreads - 1) / kThreads, 1 << 16));
@@ -2169,7 +2178,7 @@ int launch_bucket_batches(const cerar_plan *plan, const std::vector<BucketRef> &
         size_t wgs = 0;
         auto flush = [&]() -> int {
             if (b.n == 0) return CERAR_OK;
-            if (wgs > 0x7fffffffu) return fail(CERAR_E_INVAL, "bucket batch too large for one launch");
+            if (!fits_dispatch(wgs, kThreads)) return fail(CERAR_E_INVAL, "bucket batch too large for one launch");
             launch(b, pass == 0 ? Path::kFast : Path::kMaskedVec, dim3((unsigned)wgs));
             HIP_TRY(hipGetLastError(), "launch bucket batch");
             b.n = 0;
@@ -2183,6 +2192,10 @@ int launch_bucket_batches(const cerar_plan *plan, const std::vector<BucketRef> &
             int wgpw;
             size_t bpw;
             wg_for(hi - lo, wgpw, bpw);
+            if (b.n > 0 && !fits_dispatch(wgs + N * (size_t)wgpw, kThreads)) {
+                const int st = flush();
+                if (st) return st;
+            }
             set(b, b.n, bk[q], lo, hi, bpw);
             b.in[b.n].wg0 = (unsigned)wgs;
             ++b.n;
@@ -2347,26 +2360,31 @@ static int ring_simulate_bucketed_impl(const cerar_plan *plan, int nbuckets, con
         st = enqueue_encode(plan, dc, geo[b], bucket_len[b], grads + bucket_off[b], ld_grads, work + lay[b].work_off,
                             ld_work, (char *)ws + lay[b].ws_off, s);
     for (int k = 1; k < plan->L && !st; ++k) {
-        for (int b0 = 0; b0 < nbuckets; b0 += kMaxBatch) {
+        for (int b0 = 0; b0 < nbuckets;) {
             BatchRoundParams a;
             a.ops = dc->rounds + (size_t)k * N;
             a.ld_work = ld_work;
             a.Nc = plan->N * plan->c;
             a.c = plan->c;
-            a.nb = std::min(kMaxBatch, nbuckets - b0);
+            a.nb = 0;
             size_t wgs = 0;
-            for (int q = 0; q < a.nb; ++q) {
-                const BucketLayout &B = lay[b0 + q];
-                BatchInst &I = a.b[q];
+            // up to kMaxBatch buckets, as many as one dispatch holds
+            for (; b0 < nbuckets && a.nb < kMaxBatch; ++b0) {
+                const BucketLayout &B = lay[b0];
+                const unsigned wgpw = round_wgs(B.p, all_vec);
+                if (!fits_dispatch(wgs + (size_t)N * wgpw, kRoundThreads)) {
+                    if (a.nb == 0) return fail(CERAR_E_INVAL, "bucket of p=%zu is too long for one round launch", B.p);
+                    break;
+                }
+                BatchInst &I = a.b[a.nb++];
                 I.work = work + B.work_off;
                 I.pool = (float *)((char *)ws + B.ws_off);
                 I.p = B.p;
                 I.pool_stride = B.stride;
-                I.wgpw = round_wgs(B.p, all_vec);
+                I.wgpw = wgpw;
                 I.wg0 = (unsigned)wgs;
-                wgs += (size_t)N * I.wgpw;
+                wgs += (size_t)N * wgpw;
             }
-            if (wgs > 0x7fffffffu) return fail(CERAR_E_INVAL, "bucket batch too large for one launch");
             const dim3 grid((unsigned)wgs);
             const int mode = round_mode(plan, k);
             if (all_vec) {
