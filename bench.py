@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--copy-floats", type=int, default=1 << 30, help="size of the copy reference")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("TRACE_DIR", "BENCH_LOG", "OUT"),
                     help="write the summary of a rocprofv3 --kernel-trace --stats run of this bench")
+    ap.add_argument("--traced-args", default="",
+                    help="with --summarize-trace: the flags the traced bench.py run was given")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
                     help="write the HBM traffic summary of two rocprofv3 --pmc runs of this bench")
     return ap.parse_args()
@@ -112,7 +114,9 @@ def _step_bytes_cfg4():
             "k_round<2> (K3: recv - delta)": N * bw["rounds"][c]}
 
 
-def summarize_trace(trace_dir, bench_log, out_path):
+def summarize_trace(trace_dir, bench_log, out_path, bench_args=()):
+    """Summary of a rocprofv3 kernel trace of one bench.py run (bench_args:
+    the flags that run was given, recorded in the command line)."""
     stats = _read_csv(_find_csv(trace_dir, "kernel_stats.csv"))
     bench = None
     with open(bench_log) as f:
@@ -133,34 +137,43 @@ def summarize_trace(trace_dir, bench_log, out_path):
     rows.sort(key=lambda x: -x[2])
     rows.append(("other kernels (torch input generation, untimed)", other[0], other[1],
                  other[1] / max(other[0], 1), other[2]))
-    lines = ["# Kernel durations of the headline bench, rocprofv3 kernel trace",
-             "# workload: N=8 workers, c=64, d=1,414,647,808 fp32 (Pythia-1.4B-shaped), kappa_max=1e3 plan",
+    cfg = bench["config"] if bench else {}
+    name = cfg.get("workload_name", "pythia-1.4b")
+    flags = " ".join(bench_args) if bench_args else ""
+    lines = [f"# Kernel durations of bench.py on the {name} workload, rocprofv3 kernel trace",
+             f"# workload: {cfg.get('workload', '?')}; plan: {cfg.get('plan', '?')}",
              "# command (repo root, MI355X):",
-             "#   rocprofv3 --kernel-trace --stats -f csv -d gpurun_out/prof/trace -o trace -- python3 bench.py "
-             "> gpurun_out/prof/trace_bench.log",
-             "#   python3 bench.py --summarize-trace gpurun_out/prof/trace gpurun_out/prof/trace_bench.log "
-             "profiles/kernel_trace_cerar_n8_c64_pythia1.4b.txt",
+             f"#   rocprofv3 --kernel-trace --stats -f csv -d {trace_dir} -o trace -- python3 bench.py"
+             f"{' ' + flags if flags else ''} > {bench_log}",
+             f"#   python3 bench.py --summarize-trace {trace_dir} {bench_log} {out_path}",
              f"# kernel_source_sha256: {kernel_source_hash()}", "",
              f"{'kernel':<60s} {'calls':>6s} {'avg_us':>10s} {'total_ms':>10s} {'pct':>6s}"]
     fam_ns = {}
     for name, calls, tot, avg, pct in rows:
         short = name if len(name) <= 60 else name[:57] + "..."
         lines.append(f"{short:<60s} {calls:6d} {avg / 1e3:10.1f} {tot / 1e6:10.2f} {pct:6.2f}")
-        fam = family_of_name(name)
+        # the bucketed call's batch kernels are listed but kept out of the
+        # per-family comparison with the single-instance step's events
+        fam = None if "_batch" in name else family_of_name(name)
         if fam:
-            t, n = fam_ns.get(fam, (0.0, 0))
-            fam_ns[fam] = (t + tot, n + calls)
+            fam_ns.setdefault(fam, []).append((calls, tot))
     lines += ["", "# per family: trace average vs the bench's HIP-event average on the launch stream",
               f"{'family':<42s} {'trace_avg_ms':>12s} {'event_avg_ms':>12s} {'ratio':>7s}"]
-    for fam, (t, n) in fam_ns.items():
+    for fam, parts in fam_ns.items():
         ev = bench["kernels"].get(fam, {}).get("avg_ms") if bench else None
-        ta = t / n / 1e6
+        if fam in ("k_encode (K1)", "k_decode (K4)") and len({n for n, _ in parts}) == 1:
+            # one encode or decode is every listed kernel once (interior blocks,
+            # then the masked tail), and the events bracket all of them
+            ta = sum(t / n for n, t in parts) / 1e6
+        else:                       # a round is one launch of one of the listed kernels
+            ta = sum(t for _, t in parts) / sum(n for n, _ in parts) / 1e6
         lines.append(f"{fam:<42s} {ta:12.4f} {ev if ev is not None else float('nan'):12.4f} "
                      f"{(ev / ta) if ev else float('nan'):7.3f}")
     if bench:
+        rf = bench["roofline"]
         lines += ["", f"# bench line: {bench['ms_per_step']} ms/step, {bench['value']} GB/s "
                       f"({bench['config']['pct_hbm_peak']}% of 8 TB/s); roofline kernel "
-                      f"{bench['roofline']['kernel']} at {bench['roofline']['achieved']} GB/s"]
+                      f"{rf['kernel']} at {rf['achieved']} {rf.get('unit', 'GB/s')} ({rf.get('bound', 'hbm')} bound)"]
     with open(out_path, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -298,7 +311,7 @@ def cpu_baseline(wl, S):
 def main():
     args = parse()
     if args.summarize_trace:
-        summarize_trace(*args.summarize_trace)
+        summarize_trace(*args.summarize_trace, bench_args=args.traced_args.split())
         return
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, copy_floats=args.copy_floats)
@@ -439,6 +452,19 @@ def main():
         kernels[name]["mfma_frac"] = kernels[name]["tflops"] / FP32_MFMA_PEAK_TFLOPS
     dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     dk = kernels[dominant]
+    # the dominant kernel's roof: MFMA when its flops per algorithmic byte
+    # exceed the ridge of the two peaks (fp32 MFMA / HBM), else HBM
+    mfma_bound = "tflops" in dk and (
+        dk["tflops"] * 1e12 / (dk["gbps"] * 1e9) > FP32_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9))
+    if mfma_bound:
+        roofline = {"bound": "mfma", "kernel": dominant, "achieved": round(dk["tflops"], 1),
+                    "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(dk["mfma_frac"], 4),
+                    "traffic": None}
+    else:
+        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
+                    # the committed counter summary covers the headline workload only
+                    "traffic": committed_traffic(dominant) if args.workload == synth.HEADLINE else None}
 
     # achievable-bandwidth reference: a plain copy kernel
     nf = min(args.copy_floats, grads.numel())
@@ -476,13 +502,10 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "N": N, "c": c, "d": d, "p": p, "L": L,
+        "config": {"workload": wl.name, "workload_name": args.workload, "N": N, "c": c, "d": d, "p": p, "L": L,
                    "plan": plan_desc, "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
                    "bytes_per_step": step_bytes, "encode": "out of place (grads kept for every step)"},
-        "roofline": {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
-                     # the committed counter summary covers the headline workload only
-                     "traffic": committed_traffic(dominant) if args.workload == synth.HEADLINE else None},
+        "roofline": roofline,
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
         "bucketed": bucketed,

@@ -97,14 +97,20 @@ def test_trace_summary_compares_trace_and_event_averages(tmp_path):
         ['"void cerar::(anonymous namespace)::k_round<1, false>(cerar::(anonymous namespace)::RoundParams)"',
          10, 4_600_000, 460_000, 30.0],
         ['"void at::native::elementwise_kernel<128, 4>(int)"', 5, 500_000, 100_000, 10.0]])
-    line = {"ms_per_step": 65.0, "value": 5700.0, "config": {"pct_hbm_peak": 71.3},
+    line = {"ms_per_step": 65.0, "value": 5700.0,
+            "config": {"pct_hbm_peak": 71.3, "workload_name": "gpt2-small", "workload": "GPT-2-small N=8 c=32",
+                       "plan": "kappa_max=1e3"},
             "roofline": {"kernel": "k_round<1> (K3: recv - delta + delta)", "achieved": 6300.0},
             "kernels": {"k_round<1> (K3: recv - delta + delta)": {"avg_ms": 0.459}}}
     log = tmp_path / "bench.log"
     log.write_text("some text\n" + json.dumps(line) + "\n")
     out = tmp_path / "trace.txt"
-    bench.summarize_trace(str(tmp_path / "trace"), str(log), str(out))
-    rows = [r for r in out.read_text().splitlines() if r.startswith("k_round<1> (K3")]
+    bench.summarize_trace(str(tmp_path / "trace"), str(log), str(out),
+                          bench_args=["--workload", "gpt2-small", "--cpu-positions", "0"])
+    text = out.read_text()
+    assert "on the gpt2-small workload" in text and "GPT-2-small N=8 c=32; plan: kappa_max=1e3" in text
+    assert "-- python3 bench.py --workload gpt2-small --cpu-positions 0 > " in text
+    rows = [r for r in text.splitlines() if r.startswith("k_round<1> (K3")]
     assert len(rows) == 1
     trace_avg, event_avg, ratio = (float(x) for x in rows[0].split()[-3:])
     assert trace_avg == pytest.approx(0.45) and event_avg == pytest.approx(0.459)
