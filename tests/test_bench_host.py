@@ -124,3 +124,25 @@ def test_more_than_one_gpu_is_refused():
     assert run.returncode == 2
     assert "--gpus 2 is not supported" in run.stderr
     assert run.stdout.strip() == ""
+
+
+def test_committed_profiles_are_consistent():
+    """The committed counter summary covers every timed family at the
+    headline, its traffic per launch stays within 2 % below and 6 % above the
+    algorithmic bytes (no re-reads), and the traced summaries agree with the
+    bench's HIP events within 3 % for the launches that dominate the step."""
+    import re as _re
+    text = open(bench.TRAFFIC_FILE).read()
+    algo = bench._step_bytes_cfg4()
+    for fam, a in algo.items():
+        m = _re.search(r"^traffic_bytes_per_launch\[" + _re.escape(fam) + r"\]: (\d+)", text, _re.M)
+        assert m, fam
+        assert 0.98 <= int(m.group(1)) / a <= 1.06, (fam, int(m.group(1)) / a)
+    trace = open(os.path.join(ROOT, "profiles", "kernel_trace_cerar_n8_c64_pythia1.4b.txt")).read()
+    for fam in ("k_encode (K1)", "k_decode (K4)", "k_round<1> (K3: recv - delta + delta)"):
+        row = [r for r in trace.splitlines() if r.startswith(fam)]
+        assert len(row) == 1, fam
+        ratio = float(row[0].split()[-1])
+        assert 0.97 <= ratio <= 1.03, (fam, ratio)
+    for f in os.listdir(os.path.join(ROOT, "profiles")):
+        assert f.endswith((".txt", ".md")), f
