@@ -450,6 +450,12 @@ def main():
     for name, key in (("k_encode (K1)", "encode"), ("k_decode (K4)", "decode")):
         kernels[name]["tflops"] = N * flops[key] / (kernels[name]["avg_ms"] * 1e-3) / 1e12
         kernels[name]["mfma_frac"] = kernels[name]["tflops"] / FP32_MFMA_PEAK_TFLOPS
+    # per-step spans (first event to last) of the timed loop: the paper reports
+    # the median over runs (appendix, details of the numerical experiments);
+    # the value above is the mean over the timed steps
+    spans = sorted(ev[0].elapsed_time(ev[L + 2]) for ev in events)
+    step_spans = {"median": round(spans[len(spans) // 2], 4), "min": round(spans[0], 4),
+                  "max": round(spans[-1], 4)}
     dominant = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     dk = kernels[dominant]
     # the dominant kernel's roof: MFMA when its flops per algorithmic byte
@@ -508,6 +514,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "ms_per_step_ring_simulate": round(ms_ring, 4),
+        "step_ms_events": step_spans,
         "bucketed": bucketed,
         "fused_variant": fused,
         "copy_gbps": round(copy_gbps, 1),
