@@ -227,6 +227,37 @@ def test_side_stream_and_step_calls_match_single_call():
     assert bool(torch.equal(out, out2))
 
 
+def test_two_streams_share_one_plan():
+    """One plan, two independent all-reduces enqueued step by step on two
+    streams, interleaved call by call from the host, so their kernels may
+    overlap on the device: each gives the bits of the same call made alone,
+    and each workspace's step cursor follows its own stream's calls."""
+    torch, dev = torch_dev()
+    N, c, d = 8, 32, 32 * 3000 + 5
+    U, R = orthogonal_plan(N, c, seed=41)
+    plan = C.Plan.explicit(U, R)
+    ga, gb = to_device(host_grads(N, d, seed=41)), to_device(host_grads(N, d, seed=42))
+    ref = []
+    for g in (ga, gb):
+        work, ws, out = buffers(plan, d)
+        C.ring_simulate(plan, d, g, work, ws, out)
+        sync()
+        ref.append(out.clone())
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    bufs = [buffers(plan, d), buffers(plan, d)]
+    for s in (sa, sb):
+        s.wait_stream(torch.cuda.current_stream())
+    for k in range(plan.L + 1):
+        for g, s, (work, ws, _) in ((ga, sa, bufs[0]), (gb, sb, bufs[1])):
+            C.encode_round(plan, k, d, g, work, ws, stream=s)
+    for s, (work, ws, out) in ((sa, bufs[0]), (sb, bufs[1])):
+        C.decode(plan, d, work, ws, out, stream=s)
+    sa.synchronize()
+    sb.synchronize()
+    assert bool(torch.equal(bufs[0][2], ref[0]))
+    assert bool(torch.equal(bufs[1][2], ref[1]))
+
+
 def test_in_place_encode_matches_out_of_place():
     N, c, d = 4, 16, 16 * 1000
     U, R = mpc_plan(N, c, 0.3, seed=9)
