@@ -249,8 +249,40 @@ def _ptr(t):
 
 
 def _ld(t):
-    assert t.dim() == 2 and t.stride(1) == 1, "expected an (N, ld) row-major tensor"
     return t.stride(0)
+
+
+def _on_device(t, name):
+    """t must be a tensor in device memory of the current device: the kernels
+    read and write it directly."""
+    import torch
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a tensor on the GPU")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} is on cuda:{t.device.index}, the current device is "
+                         f"cuda:{torch.cuda.current_device()}")
+
+
+def _rows(t, name, rows, cols, dtype="float32"):
+    """t must be an (at least rows x cols) row-major tensor of `dtype`, so
+    that every element the kernels touch through (pointer, row stride) lies
+    inside it."""
+    _on_device(t, name)
+    if str(t.dtype) != "torch." + dtype:
+        raise ValueError(f"{name} must be {dtype}, not {t.dtype}")
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{name} must be a 2-D row-major tensor (unit column stride)")
+    if t.shape[0] < rows or t.shape[1] < cols:
+        raise ValueError(f"{name} has shape {tuple(t.shape)}; at least ({rows}, {cols}) is needed")
+
+
+def _bytes(t, name, nbytes):
+    """t must be a contiguous device tensor of at least nbytes bytes."""
+    _on_device(t, name)
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes; {nbytes} are needed")
 
 
 def allocate(plan, d, device="cuda", work_like_grads=False):
@@ -264,28 +296,51 @@ def allocate(plan, d, device="cuda", work_like_grads=False):
     return work, ws, out
 
 
+def _step_buffers(plan, d, grads=None, work=None, ws=None, out=None):
+    p, _ = plan.chunk_len(d)
+    if grads is not None:
+        _rows(grads, "grads", plan.N, d)
+    if work is not None:
+        _rows(work, "work", plan.N, plan.c * p)
+    if ws is not None:
+        _bytes(ws, "ws", plan.workspace_bytes(d))
+    if out is not None:
+        _rows(out, "out", plan.N, d)
+
+
 def encode_round(plan, step, d, grads, work, ws, stream=None):
+    _step_buffers(plan, d, grads, work, ws)
     _check(lib().cerar_encode_round(plan.handle, step, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
                                     _ptr(ws), _stream(stream)))
 
 
 def decode(plan, d, work, ws, out, stream=None):
+    _step_buffers(plan, d, None, work, ws, out)
     _check(lib().cerar_decode(plan.handle, d, _ptr(work), _ld(work), _ptr(ws), _ptr(out), _ld(out),
                               _stream(stream)))
 
 
 def ring_simulate(plan, d, grads, work, ws, out, stream=None):
+    _step_buffers(plan, d, grads, work, ws, out)
     _check(lib().cerar_ring_simulate(plan.handle, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
                                      _ptr(ws), _ptr(out), _ld(out), _stream(stream)))
 
 
 def ring_simulate_fused(plan, d, grads, out, stream=None):
     """The single-GPU fused variant (cerar_ring_simulate_fused)."""
+    _rows(grads, "grads", plan.N, d)
+    _rows(out, "out", plan.N, d)
     _check(lib().cerar_ring_simulate_fused(plan.handle, d, _ptr(grads), _ld(grads), _ptr(out), _ld(out),
                                            _stream(stream)))
 
 
 def ring_simulate_bucketed(plan, buckets, grads, work, ws, out, stream=None):
+    span = max((b[0] + b[1] for b in buckets), default=0)
+    work_floats, ws_bytes = plan.bucketed_sizes([b[1] for b in buckets])
+    _rows(grads, "grads", plan.N, span)
+    _rows(work, "work", plan.N, work_floats)
+    _bytes(ws, "ws", ws_bytes)
+    _rows(out, "out", plan.N, span)
     offs = (_SZ * len(buckets))(*[b[0] for b in buckets])
     lens = (_SZ * len(buckets))(*[b[1] for b in buckets])
     _check(lib().cerar_ring_simulate_bucketed(plan.handle, len(buckets), offs, lens, _ptr(grads), _ld(grads),
@@ -294,12 +349,22 @@ def ring_simulate_bucketed(plan, buckets, grads, work, ws, out, stream=None):
 
 
 def error_norms(N, d, grads, out, norms, stream=None):
+    _rows(grads, "grads", N, d)
+    _rows(out, "out", N, d)
+    _on_device(norms, "norms")
+    if str(norms.dtype) != "torch.float64" or not norms.is_contiguous() or norms.numel() < N + 1:
+        raise ValueError(f"norms must be a contiguous float64 tensor of at least {N + 1} entries")
     _check(lib().cerar_error_norms(N, d, _ptr(grads), _ld(grads), _ptr(out), _ld(out), _ptr(norms),
                                    _stream(stream)))
 
 
 def copy_f32(dst, src, stream=None):
-    assert dst.numel() == src.numel()
+    for t, name in ((dst, "dst"), (src, "src")):
+        _on_device(t, name)
+        if str(t.dtype) != "torch.float32" or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 tensor")
+    if dst.numel() != src.numel():
+        raise ValueError(f"dst has {dst.numel()} elements, src {src.numel()}")
     _check(lib().cerar_copy_f32(_ptr(dst), _ptr(src), dst.numel(), _stream(stream)))
 
 

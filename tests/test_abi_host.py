@@ -312,3 +312,25 @@ def test_slot_map_handoffs(N, c):
     assert len(used) <= nslots
     pool_used = {s for s in used if s >= N * c}
     assert len(pool_used) == N * N
+
+
+def test_binding_refuses_host_tensors():
+    """The Python binding passes raw pointers to kernels, so it refuses
+    tensors outside device memory before any library call."""
+    import torch
+    plan = C.Plan(4, 4, "o_eps", 0.1, seed=1)
+    d = 100
+    work_floats = plan.c * plan.chunk_len(d)[0]
+    g = torch.zeros((4, d))
+    w = torch.zeros((4, work_floats))
+    ws = torch.zeros(plan.workspace_bytes(d), dtype=torch.uint8)
+    out = torch.zeros((4, d))
+    for call in (lambda: C.ring_simulate(plan, d, g, w, ws, out),
+                 lambda: C.encode_round(plan, 0, d, g, w, ws),
+                 lambda: C.decode(plan, d, w, ws, out),
+                 lambda: C.ring_simulate_fused(plan, d, g, out),
+                 lambda: C.ring_simulate_bucketed(plan, [(0, d)], g, w, ws, out),
+                 lambda: C.error_norms(4, d, g, out, torch.zeros(5, dtype=torch.float64)),
+                 lambda: C.copy_f32(out, g)):
+        with pytest.raises(ValueError, match="must be a tensor on the GPU"):
+            call()

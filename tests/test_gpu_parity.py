@@ -258,6 +258,36 @@ def test_two_streams_share_one_plan():
     assert bool(torch.equal(bufs[1][2], ref[1]))
 
 
+def test_binding_checks_dtype_layout_and_extent():
+    """Tensors the kernels would read or write out of range, or in the wrong
+    element type, are refused by the binding before any launch."""
+    torch, dev = torch_dev()
+    N, c, d = 4, 8, 8 * 300 + 3
+    U, R = orthogonal_plan(N, c, seed=5)
+    plan = C.Plan.explicit(U, R)
+    grads = to_device(host_grads(N, d, seed=5))
+    work, ws, out = buffers(plan, d)
+    bad = [
+        ("grads must be float32", lambda: C.ring_simulate(plan, d, grads.double(), work, ws, out)),
+        ("grads has shape", lambda: C.ring_simulate(plan, d, grads[:N - 1], work, ws, out)),
+        ("grads has shape", lambda: C.ring_simulate(plan, d + 1, grads, work, ws, out)),
+        ("work has shape", lambda: C.encode_round(plan, 0, d, grads, work[:, :-1], ws)),
+        ("ws holds", lambda: C.ring_simulate(plan, d, grads, work, ws[:-4], out)),
+        ("ws must be contiguous", lambda: C.ring_simulate(plan, d, grads, work, ws.view(2, -1).t(), out)),
+        ("out has shape", lambda: C.decode(plan, d, work, ws, out[:, :d - 1])),
+        ("row-major", lambda: C.ring_simulate(plan, d, grads, work, ws, out.t().contiguous().t())),
+        ("out has shape", lambda: C.ring_simulate_fused(plan, d, grads, out[1:])),
+        ("norms must be", lambda: C.error_norms(N, d, grads, out, torch.zeros(N, dtype=torch.float64, device=dev))),
+        ("dst has", lambda: C.copy_f32(out.view(-1)[:-1], grads.view(-1))),
+    ]
+    before = out.clone()
+    for what, call in bad:
+        with pytest.raises(ValueError, match=what):
+            call()
+    sync()
+    assert bool(torch.equal(out.isnan(), before.isnan()))
+
+
 def test_in_place_encode_matches_out_of_place():
     N, c, d = 4, 16, 16 * 1000
     U, R = mpc_plan(N, c, 0.3, seed=9)
