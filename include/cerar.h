@@ -25,7 +25,8 @@
  *    (NULL = the legacy default stream); they never synchronise, with one
  *    exception: the first such call for a plan on a device uploads the
  *    plan's fp32 coefficients and tables to that device (hipMalloc and a
- *    synchronous hipMemcpy, once per plan and device).  After it, the calls
+ *    synchronous hipMemcpy, once per plan and device), unless
+ *    cerar_plan_prepare_device did so before.  After it, the calls
  *    issue kernel launches only (no allocation, copy or memset), so they can
  *    be recorded into a HIP graph by stream capture.  Work enqueued by calls
  *    that share buffers must be ordered by the caller (one stream does
@@ -141,6 +142,16 @@ int cerar_plan_create_explicit(int N, int c, const double *U, const double *R,
 
 /* Frees host and device memory of the plan.  No work using it may be pending. */
 void cerar_plan_destroy(cerar_plan *plan);
+
+/* Uploads the plan's fp32 coefficient fragments and slot tables to the
+ * current device, once per plan and device (hipMalloc and a synchronous
+ * hipMemcpy); later calls for that device return at once.  Every enqueueing
+ * call does this itself on its first use on a device.  Calling it first lets
+ * a caller record those calls into a HIP graph by stream capture without an
+ * eager call, since after it they issue kernel launches only.  Thread-safe.
+ * Errors: E_INVAL (NULL plan); E_DEVICE (a HIP call failed; nothing is kept
+ * for that device). */
+int cerar_plan_prepare_device(const cerar_plan *plan);
 
 int cerar_plan_get_info(const cerar_plan *plan, cerar_plan_info *info);
 

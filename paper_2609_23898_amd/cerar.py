@@ -61,6 +61,7 @@ SIGNATURES = {
     "cerar_plan_create_explicit": (_I, [_I, _I, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_P)]),
     "cerar_plan_destroy": (None, [_P]),
+    "cerar_plan_prepare_device": (_I, [_P]),
     "cerar_plan_get_info": (_I, [_P, ctypes.POINTER(PlanInfo)]),
     "cerar_plan_get_matrices": (_I, [_P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
     "cerar_chunk_len": (_I, [_P, _SZ, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]),
@@ -187,6 +188,11 @@ class Plan:
         R = np.empty((self.N, self.L + 1, self.c))
         _check(lib().cerar_plan_get_matrices(self._h, _dptr(U.ctypes.data), _dptr(R.ctypes.data)))
         return U, R
+
+    def prepare_device(self):
+        """Upload the plan to the current device now (cerar_plan_prepare_device),
+        so that the enqueueing calls can be captured into a HIP graph."""
+        _check(lib().cerar_plan_prepare_device(self._h))
 
     def chunk_len(self, d):
         p, s = _SZ(), _SZ()

@@ -1879,6 +1879,15 @@ void release_device(cerar_plan *plan) {
 
 using namespace cerar;
 
+extern "C" int cerar_plan_prepare_device(const cerar_plan *plan) {
+    clear_error();
+    if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
+    return guarded([&] {
+        const DeviceCopy *dc;
+        return device_copy(plan, &dc);
+    });
+}
+
 static int encode_round_impl(const cerar_plan *plan, int step, size_t d, const float *grads,
                              size_t ld_grads, float *work, size_t ld_work, void *ws, cerar_stream stream) {
     Geometry g;

@@ -29,7 +29,7 @@ def header_functions():
 
 def test_library_exports_every_declared_function():
     names = header_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     lib = C.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -262,6 +262,7 @@ def test_device_calls_validate_before_touching_the_device():
     assert lib.cerar_ring_simulate(plan.handle, 0, fake, 1, fake, 1, ws, out, 1, None) == -1
     assert lib.cerar_error_norms(0, 10, fake, 10, out, 10, ws, None) == -1
     assert lib.cerar_copy_f32(None, fake, 10, None) == -1
+    assert lib.cerar_plan_prepare_device(None) == -1
     # overlapping buckets
     offs = (ctypes.c_size_t * 2)(0, 100)
     lens = (ctypes.c_size_t * 2)(200, 200)

@@ -7,14 +7,15 @@ torch.cuda.graph can capture them.  Every replay runs on fresh inputs copied
 into the captured buffers, with an eager call of the same entry point on
 separate buffers and a synchronisation between replays, and must give
 exactly the eager result; the first replay is also checked against the
-oracle."""
+oracle.  cerar_plan_prepare_device makes the eager call unnecessary: the
+last test records the first call made on the device."""
 
 import numpy as np
 import pytest
 
 from paper_2609_23898_amd import cerar as C
 
-from gpu_util import buffers, host_grads, max_rel_l2, oracle_allreduce, orthogonal_plan, torch_dev
+from gpu_util import buffers, host_grads, max_rel_l2, oracle_allreduce, orthogonal_plan, to_device, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -122,3 +123,26 @@ def test_fused_variant_replays_from_a_graph():
 
     inputs = [host_grads(N, d, seed=330 + r) for r in range(REPLAYS)]
     _check_replays(call, make_bufs, inputs, d, oracle_check)
+
+
+def test_prepared_plan_captures_without_an_eager_call():
+    """After cerar_plan_prepare_device the very first call on the device can
+    be the one recorded into the graph."""
+    torch, dev = torch_dev()
+    N, c, d = 4, 16, 16 * 512 + 3
+    U, R = orthogonal_plan(N, c, seed=34)
+    plan = C.Plan.explicit(U, R)
+    plan.prepare_device()
+    plan.prepare_device()                       # a second call is a no-op
+    g = host_grads(N, d, seed=34)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        C.ring_simulate(plan, d, grads, work, ws, out)
+    for _ in range(2):
+        out.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert max_rel_l2(out.double().cpu().numpy(), oracle_allreduce(g, U, R)) <= 1e-4
+    del graph
