@@ -202,7 +202,9 @@ int cerar_slot_map(const cerar_plan *plan, int step, int *slots);
  * Steps must run in order 0, 1, .., L on the same (work, ws) with the same
  * d: the library keeps the next expected step and the encode's d per
  * workspace address and returns E_STATE otherwise (step 0 is always accepted
- * and restarts the sequence). */
+ * and restarts the sequence).  That record, a few dozen bytes per workspace
+ * address used with the plan, is kept until cerar_plan_destroy; the order is
+ * checked at enqueue time, which is also the order on one stream. */
 int cerar_encode_round(const cerar_plan *plan, int step, size_t d,
                        const float *grads, size_t ld_grads,
                        float *work, size_t ld_work, void *ws, cerar_stream stream);
