@@ -205,11 +205,10 @@ def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30):
              "# workload: N=8 workers, c=64, d=1,414,647,808 fp32 (Pythia-1.4B-shaped), kappa_max=1e3 plan",
              "# commands (repo root, MI355X), one counter per run:",
              "#   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
-             "-d gpurun_out/prof/fetch -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
+             f"-d {fetch_dir} -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
              "#   rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
-             "-d gpurun_out/prof/write -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
-             "#   python3 bench.py --summarize-pmc gpurun_out/prof/fetch gpurun_out/prof/write "
-             "profiles/hbm_traffic_cerar_n8_c64_pythia1.4b.txt",
+             f"-d {write_dir} -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
+             f"#   python3 bench.py --summarize-pmc {fetch_dir} {write_dir} {out_path}",
              "# scale: each counter divided by what it reads for the plain copy kernel k_copy4 moving "
              f"{copy_floats} floats ({copy_kib:.0f} KiB read and written per dispatch)",
              f"kernel_source_sha256: {kernel_source_hash()}",
