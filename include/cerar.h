@@ -250,7 +250,11 @@ int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *gra
  * workers, then every bucket's decode.  With c <= 64 and 16-byte aligned
  * rows in every bucket, the encode and the decode are batched as well (up to
  * 32 buckets per launch); otherwise each bucket gets its own launches.
- * bucket_off/bucket_len are host arrays; buckets may not overlap in out. */
+ * bucket_off/bucket_len are host arrays; buckets may not overlap in out.
+ * Errors: E_INVAL (NULL plan or buffers, nbuckets < 1, an empty bucket,
+ * overlapping buckets, ld_work below the slot total, ld_grads or ld_out below
+ * the largest bucket end, out overlapping work or ws, grads overlapping
+ * work, or a bucket too long for one launch); E_DEVICE. */
 int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len,
                                    int nbuckets, size_t *work_floats, size_t *ws_bytes);
 int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,
@@ -262,14 +266,16 @@ int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,
 /* Error norms (the metric of Table 3, relative l2 error per worker):
  * norms (device, N+1 doubles) receives sum_e (out_i[e] - S[e])^2 for
  * i = 0..N-1, then sum_e S[e]^2, where S = sum_w grads_w (fp64) over
- * e < d.  Overwrites norms. */
+ * e < d.  Overwrites norms.  Errors: E_INVAL (N outside [1, 64], d == 0,
+ * NULL buffers, ld_grads or ld_out < d); E_DEVICE. */
 int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_grads,
                       const float *out, size_t ld_out, double *norms,
                       cerar_stream stream);
 
 /* Measurement helper: dst[0..n) = src[0..n), a plain streaming copy used as
  * the achievable-bandwidth reference and as the known-size kernel that
- * scales the HBM traffic counters. */
+ * scales the HBM traffic counters.  n == 0 does nothing.  Errors: E_INVAL
+ * (NULL or overlapping buffers, a copy too long for one launch); E_DEVICE. */
 int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stream stream);
 
 /* Text of the calling thread's last non-OK status ("" if none). */
