@@ -9,6 +9,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libcerar.so")
+EXAMPLE_SRC = os.path.join(ROOT, "tests", "c_abi", "allreduce.c")
+EXAMPLE = os.path.join(ROOT, "tests", "c_abi", "allreduce")
 
 HIP_SOURCES = ["kernels.hip"]
 CXX_SOURCES = ["plan.cpp", "linalg.cpp"]
@@ -46,8 +48,12 @@ def build(verbose=False):
     tmp_out = OUT + ".tmp"
     _run([hipcc, "-shared", "--offload-arch=gfx950", "-fPIC", *objs, "-o", tmp_out, "-lpthread"])
     os.replace(tmp_out, OUT)
+    # a C consumer of the ABI alone (no Python), run by the GPU tests
+    _run(["gcc", "-std=c11", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+          "-I", "/opt/rocm/include", EXAMPLE_SRC, "-o", EXAMPLE, "-L", HERE, "-lcerar",
+          "-L", "/opt/rocm/lib", "-lamdhip64", "-lm", "-Wl,-rpath,$ORIGIN/../../paper_2609_23898_amd", "-Wl,-rpath,/opt/rocm/lib"])
     if verbose:
-        print("built", OUT)
+        print("built", OUT, "and", EXAMPLE)
     return OUT
 
 
