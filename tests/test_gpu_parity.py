@@ -288,6 +288,47 @@ def test_binding_checks_dtype_layout_and_extent():
     assert bool(torch.equal(out.isnan(), before.isnan()))
 
 
+def test_host_threads_share_one_fresh_plan():
+    """Four host threads make their first calls on one plan at the same time
+    (the one-time device upload and the per-workspace step records are
+    shared state), each stepping its own all-reduce on its own stream; each
+    result equals the single call made afterwards on the same inputs."""
+    import threading
+    torch, dev = torch_dev()
+    N, c, d = 4, 16, 16 * 2000 + 3
+    U, R = orthogonal_plan(N, c, seed=51)
+    plan = C.Plan.explicit(U, R)                   # not yet on the device
+    inputs = [to_device(host_grads(N, d, seed=510 + t)) for t in range(4)]
+    bufs = [buffers(plan, d) for _ in range(4)]
+    streams = [torch.cuda.Stream() for _ in range(4)]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    start, errors = threading.Barrier(4), []
+
+    def worker(t):
+        try:
+            work, ws, out = bufs[t]
+            start.wait()
+            for k in range(plan.L + 1):
+                C.encode_round(plan, k, d, inputs[t], work, ws, stream=streams[t])
+            C.decode(plan, d, work, ws, out, stream=streams[t])
+            streams[t].synchronize()
+        except Exception as e:                     # reported below
+            errors.append((t, repr(e)))
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(4)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=120)
+    assert not errors, errors
+    for t in range(4):
+        work, ws, out = buffers(plan, d)
+        C.ring_simulate(plan, d, inputs[t], work, ws, out)
+        sync()
+        assert bool(torch.equal(bufs[t][2], out)), t
+
+
 def test_in_place_encode_matches_out_of_place():
     N, c, d = 4, 16, 16 * 1000
     U, R = mpc_plan(N, c, 0.3, seed=9)
