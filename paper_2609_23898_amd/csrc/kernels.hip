@@ -219,10 +219,16 @@ __device__ inline void mtile2_mma_lds2(v4f (&acc)[2][2], const v2f (&b)[KS], con
                                        int lane) {
 #pragma unroll
     for (int m = 0; m < 2; ++m) acc[m][0] = acc[m][1] = v4f{0.f, 0.f, 0.f, 0.f};
+    constexpr int NQ = (KS + 3) / 4;
+    v4f n0 = *reinterpret_cast<const v4f *>(sfr0 + (size_t)lane * 4);
+    v4f n1 = *reinterpret_cast<const v4f *>(sfr1 + (size_t)lane * 4);
 #pragma unroll
-    for (int q = 0; q < (KS + 3) / 4; ++q) {
-        const v4f a0 = *reinterpret_cast<const v4f *>(sfr0 + ((size_t)q * 64 + lane) * 4);
-        const v4f a1 = *reinterpret_cast<const v4f *>(sfr1 + ((size_t)q * 64 + lane) * 4);
+    for (int q = 0; q < NQ; ++q) {
+        const v4f a0 = n0, a1 = n1;                 // this K-quad's fragments; the next quad's load now
+        if (q + 1 < NQ) {
+            n0 = *reinterpret_cast<const v4f *>(sfr0 + ((size_t)(q + 1) * 64 + lane) * 4);
+            n1 = *reinterpret_cast<const v4f *>(sfr1 + ((size_t)(q + 1) * 64 + lane) * 4);
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int ks = q * 4 + r;
