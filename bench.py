@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 METRIC = "encode+round+decode GB/s per worker (% HBM peak), N=8 c=64 d=1.4e9 fp32"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+CPU_WORKERS_MAX = 15
 
 
 def log(msg):
@@ -48,8 +49,10 @@ def parse():
     ap.add_argument("--workload", default=synth.HEADLINE, choices=synth.WORKLOADS,
                     help="synthetic workload (default: the headline, pythia-1.4b)")
     ap.add_argument("--plan-iters", type=int, default=100, help="ALS iterations of the kappa design")
-    ap.add_argument("--cpu-positions", type=int, default=1 << 21,
-                    help="positions of the bounded oracle sample (0 = skip cpu_baseline)")
+    ap.add_argument("--cpu-positions", type=int, default=1 << 14,
+                    help="sampled positions per oracle process (0 = skip cpu_baseline)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="seconds each oracle process runs its sample (repeating it)")
     ap.add_argument("--copy-floats", type=int, default=1 << 30, help="size of the copy reference")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("TRACE_DIR", "BENCH_LOG", "OUT"),
                     help="write the summary of a rocprofv3 --kernel-trace --stats run of this bench")
@@ -125,7 +128,7 @@ def summarize_trace(trace_dir, bench_log, out_path, bench_args=()):
                 bench = json.loads(line)
     rows, other = [], [0, 0.0, 0.0]
     for r in stats:
-        if "cerar::" not in r["Name"]:          # torch and runtime kernels: synthetic inputs, copies
+        if "cerar::" not in r["Name"] or "k_synth_fill" in r["Name"]:   # input generation, torch copies
             other[0] += int(r["Calls"])
             other[1] += float(r["TotalDurationNs"])
             other[2] += float(r["Percentage"])
@@ -135,7 +138,7 @@ def summarize_trace(trace_dir, bench_log, out_path, bench_args=()):
         rows.append((name, int(r["Calls"]), float(r["TotalDurationNs"]), float(r["AverageNs"]),
                      float(r["Percentage"])))
     rows.sort(key=lambda x: -x[2])
-    rows.append(("other kernels (torch input generation, untimed)", other[0], other[1],
+    rows.append(("other kernels (input generation, torch copies; untimed)", other[0], other[1],
                  other[1] / max(other[0], 1), other[2]))
     cfg = bench["config"] if bench else {}
     name = cfg.get("workload_name", "pythia-1.4b")
@@ -263,48 +266,160 @@ def family_of(k, N, c, L):
     return None
 
 
-def cpu_baseline(wl, S):
-    """Time the fp64 oracle (its own plan) on S sampled positions of the
-    same workload, on one host thread."""
+def _oracle_worker(name, pos, U, R, seconds, barrier, queue):
+    """One host process of the CPU baseline: draws the oracle's inputs at its
+    positions from the shared generator, waits for the other processes, then
+    runs the fp64 oracle (encode, Algorithm 1 in lock-step, decode) on one
+    thread, repeatedly until `seconds` have passed."""
     import numpy as np
-    import torch
     from threadpoolctl import threadpool_limits
 
-    from oracle import plan as OP
+    from oracle import ring as OR
+    from paper_2609_23898_amd import synth
+    try:
+        wl = synth.workload(name)
+        N, c = wl.N, wl.c
+        p = OR.chunk_len(wl.d, c, 32)               # the library's chunk length (cerar_chunk_len)
+        flat = (np.arange(c)[None, :] * p + pos[:, None]).astype(np.int64)
+        G = [wl.values_np(w, flat.ravel()).reshape(flat.shape).astype(np.float64) for w in range(N)]
+        barrier.wait()
+        reps, finite = 0, True
+        with threadpool_limits(limits=1):
+            t0 = time.time()
+            while True:
+                out = OR.allreduce_chunks(G, U, R)
+                reps += 1
+                t1 = time.time()
+                if t1 - t0 >= seconds:
+                    break
+        finite = all(bool(np.all(np.isfinite(o))) for o in out)
+        queue.put((t0, t1, reps * len(pos), finite, None))
+    except Exception as e:                          # reported by the parent
+        try:
+            barrier.abort()
+        except Exception:
+            pass
+        queue.put((0.0, 0.0, 0, False, repr(e)))
+
+
+def cpu_baseline(name, U, R, plan_desc, positions, seconds):
+    """Time the fp64 oracle on the GPU line's own plan (U, R from the
+    library's plan) over sampled positions of the same workload: one worker
+    process per host core of the machine's CPU share, each single-threaded on its
+    own positions.  Runs before the process touches the GPU, so the workers
+    are plain forks of a process with no device state."""
+    import multiprocessing as mp
+
+    import numpy as np
+
     from oracle import ring as OR
     from paper_2609_23898_amd import synth
 
+    wl = synth.workload(name)
     N, c, d = wl.N, wl.c, wl.d
-    p = OR.chunk_len(d, c, 32)                   # the library's chunk length (cerar_chunk_len)
+    p = OR.chunk_len(d, c, 32)
+    cores = os.cpu_count() or 1
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = cores
+    # at most 15 workers: with the parent, within the 16 processes a one-GPU box allows
+    threads = max(1, min(usable, CPU_WORKERS_MAX))
     rng = np.random.default_rng(12345)
-    pos = np.unique(np.concatenate([rng.integers(0, p, size=S - 1), [p - 1]]))
-    S = pos.size
-    flat = (np.arange(c)[None, :] * p + pos[:, None]).astype(np.int64)       # S x c
-    # the shared generator gives the same bits on any device; run it on the GPU
-    idx = torch.from_numpy(flat.ravel()).to("cuda:0")
-    G = [wl.values_torch(w, idx).cpu().numpy().reshape(S, c).astype(np.float64) for w in range(N)]
-    del idx
-    with threadpool_limits(limits=1):
-        if wl.c == 64 or wl.c == 32:
-            B = synth.base_matrix(1000 + N, N, c)
-            U, R = OP.kappa_design(B, np.diag(OP.chebyshev_nodes(c)), 0.3, 1e3, 20, order="projected")
-            plan_desc = "oracle kappa design (20 ALS iterations)"
-        else:
-            B = synth.base_matrix(1000 + N, N, c)
-            U, R = OP.mpc_plan(B, OP.o_eps_perturbation(np.diag(OP.chebyshev_nodes(c)), 0.3))
-            plan_desc = "oracle O(eps) plan"
-        t0 = time.perf_counter()
-        out = OR.allreduce_chunks(G, U, R)
-        dt = time.perf_counter() - t0
-    assert all(np.all(np.isfinite(o)) for o in out)
-    bytes_sample = N * (8 * c + 3 * N - 9) * S * 4
+    per = max(1, min(positions, p // threads))
+    pos_all = np.unique(np.concatenate([rng.integers(0, p, size=per * threads - 1), [p - 1]]))
+    parts = np.array_split(pos_all, threads)
+    ctx = mp.get_context("fork")
+    barrier, queue = ctx.Barrier(threads), ctx.Queue()
+    procs = [ctx.Process(target=_oracle_worker, args=(name, part, U, R, seconds, barrier, queue))
+             for part in parts]
+    for pr in procs:
+        pr.start()
+    res = [queue.get(timeout=600) for _ in procs]
+    for pr in procs:
+        pr.join()
+    errors = [r[4] for r in res if r[4]]
+    if errors:
+        raise RuntimeError(f"cpu_baseline worker failed: {errors[0]}")
+    assert all(r[3] for r in res), "oracle output is not finite"
+    per_pos = N * (8 * c + 3 * N - 9) * 4           # algorithmic bytes per position, all workers
+    wall = max(r[1] for r in res) - min(r[0] for r in res)
+    done = sum(r[2] for r in res)
+    rates = sorted(r[2] * per_pos / (r[1] - r[0]) / 1e9 for r in res)
     step_bytes = N * (8 * c + 3 * N - 9) * p * 4
-    return {"value": bytes_sample / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "seconds": dt, "extrapolated_step_s": round(dt * step_bytes / bytes_sample, 1),
-            "sample": f"{S} positions x {c} chunks x {N} workers of the same workload "
-                      f"({S / p:.2e} of the positions), fp64 NumPy oracle "
-                      f"(encode, Algorithm 1 lock-step, decode) with its {plan_desc}; "
-                      f"GB/s counts the same algorithmic bytes per position as the GPU line"}
+    value = done * per_pos / wall / 1e9
+    return {"value": round(value, 4), "unit": "GB/s", "cores": cores, "threads": threads, "kind": "oracle",
+            "seconds": round(wall, 2), "per_thread_gbps_median": round(rates[len(rates) // 2], 4),
+            "extrapolated_step_s": round(step_bytes / (value * 1e9), 1),
+            "plan": "the GPU line's plan (its fp64 U and R, from cerar_plan_get_matrices)",
+            "sample": f"{len(pos_all)} sampled positions x {c} chunks x {N} workers of the same workload, split "
+                      f"over {threads} single-threaded processes (box: {cores} cores), each running the fp64 NumPy "
+                      f"oracle (encode, Algorithm 1 lock-step, decode) on its positions repeatedly for "
+                      f"{seconds:g} s ({done} positions in all); plan: {plan_desc}; GB/s counts the same "
+                      f"algorithmic bytes per position as the GPU line"}
+
+
+def _span_stats(xs):
+    xs = sorted(xs)
+    return {"median": round(xs[len(xs) // 2], 4), "min": round(xs[0], 4), "max": round(xs[-1], 4),
+            "mean": round(sum(xs) / len(xs), 4)}
+
+
+def in_place_steps(C, plan, d, grads, work, ws, out, steps):
+    """Steps with work == grads: before each step the work rows are refilled
+    with the gradients (and the zero pad) by the copy kernel; events bracket
+    encode..decode only.  Returns the per-step spans and the encode times."""
+    import torch
+    N, c = plan.N, plan.c
+    p, _ = plan.chunk_len(d)
+    spans, enc = [], []
+    for s in range(steps + 1):                     # the first step warms up
+        for w in range(N):
+            C.copy_f32(work[w, :d], grads[w])
+        if c * p > d:
+            work[:, d:c * p].zero_()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record()
+        C.encode_round(plan, 0, d, work, work, ws)
+        ev[1].record()
+        for k in range(1, plan.L + 1):
+            C.encode_round(plan, k, d, work, work, ws)
+        C.decode(plan, d, work, ws, out)
+        ev[2].record()
+        torch.cuda.synchronize()
+        if s > 0:
+            spans.append(ev[0].elapsed_time(ev[2]))
+            enc.append(ev[0].elapsed_time(ev[1]))
+    return {"steps": steps, "ms_per_step_events": _span_stats(spans), "encode_ms": _span_stats(enc),
+            "note": "work == grads (Sec. II storage rule); gradients restored by a copy before each step, "
+                    "outside the events"}
+
+
+def encode_spread(C, plan, d, grads, work, ws, reps):
+    """The out-of-place encode timed on the bench's gradient buffer and on a
+    second, freshly allocated copy of it (the encode's rate depends on the
+    physical backing of the allocation it reads)."""
+    import torch
+    second = torch.empty_like(grads)
+    for w in range(plan.N):
+        C.copy_f32(second[w], grads[w])
+    res = {}
+    for name, g in (("bench_buffer", grads), ("fresh_buffer", second)):
+        C.encode_round(plan, 0, d, g, work, ws)
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            C.encode_round(plan, 0, d, g, work, ws)
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        res[name] = _span_stats(ts)
+    del second
+    torch.cuda.empty_cache()
+    allv = [res[k]["median"] for k in res]
+    res["min_ms"], res["max_ms"] = min(allv), max(allv)
+    return res
 
 
 def main():
@@ -325,23 +440,32 @@ def main():
     from paper_2609_23898_amd import cerar as C
     from paper_2609_23898_amd import synth
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
-    dev = "cuda:0"
     wl = synth.workload(args.workload)
     N, c, d = wl.N, wl.c, wl.d
     t = time.perf_counter()
-    plan, plan_desc = product_plan(C, wl, args.plan_iters)
+    plan, plan_desc = product_plan(C, wl, args.plan_iters)          # host fp64, no device call
     info = plan.info()
     log(f"plan: {plan_desc} kappa_M={info['kappa_M']:.3g} phi={info['phi']:.4g} "
         f"({time.perf_counter() - t:.1f}s)")
     L = plan.L
     p, _ = plan.chunk_len(d)
+    # the oracle on the host cores, before this process touches the GPU
+    cpu = None
+    if args.cpu_positions > 0:
+        t = time.perf_counter()
+        U_plan, R_plan = plan.matrices()
+        cpu = cpu_baseline(args.workload, U_plan, R_plan, plan_desc, args.cpu_positions, args.cpu_seconds)
+        log(f"cpu baseline: {cpu['value']:.3f} GB/s on {cpu['threads']} processes "
+            f"({time.perf_counter() - t:.1f}s total)")
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
 
     t = time.perf_counter()
     grads = torch.empty((N, d), dtype=torch.float32, device=dev)
     for w in range(N):
-        wl.fill_torch(grads[w], w)
+        C.synth_fill(grads[w], wl, w)               # K6: the seeded generator on the device
     work, ws, out = C.allocate(plan, d, dev)
     torch.cuda.synchronize()
     log(f"inputs: N={N} c={c} d={d} p={p} L={L} generated in {time.perf_counter() - t:.1f}s; "
@@ -485,6 +609,17 @@ def main():
     torch.cuda.synchronize()
     copy_gbps = 2 * nf * 4 * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
+    # the paper's storage rule (Sec. II, initialisation: Delta_i overwrites G_i):
+    # the same step with the encode in place, on the work buffer refilled from
+    # the gradients before every step, outside the step's event span
+    in_place = in_place_steps(C, plan, d, grads, work, ws, out, max(1, min(args.steps, 20)))
+    log(f"in-place encode: {in_place['ms_per_step_events']['median']:.3f} ms/step (event spans), "
+        f"encode {in_place['encode_ms']['median']:.3f} ms")
+    # the encode's spread over gradient allocations: the same encode on a
+    # second, freshly allocated copy of the gradients
+    spread = encode_spread(C, plan, d, grads, work, ws, 10)
+    log(f"encode on two gradient allocations: {spread}")
+
     # approximation error of the decoded sums (K5, not timed)
     C.ring_simulate(plan, d, grads, work, ws, out)
     norms = torch.empty(N + 1, dtype=torch.float64, device=dev)
@@ -516,6 +651,8 @@ def main():
         "step_ms_events": step_spans,
         "bucketed": bucketed,
         "fused_variant": fused,
+        "in_place_encode": in_place,
+        "encode_spread": spread,
         "copy_gbps": round(copy_gbps, 1),
         "approx_rel_err_max": max(rel_err),
         "plan_info": {k: info[k] for k in ("kappa_M", "kappa_U", "kappa_R", "phi", "phi_closed_form",
@@ -523,10 +660,8 @@ def main():
     }
     del grads, work, ws, out
     torch.cuda.empty_cache()
-    if args.cpu_positions > 0:
-        t = time.perf_counter()
-        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_positions)
-        log(f"cpu baseline: {result['cpu_baseline']['value']:.3f} GB/s ({time.perf_counter() - t:.1f}s total)")
+    if cpu is not None:
+        result["cpu_baseline"] = cpu
     for k, v in list(result["plan_info"].items()):
         if isinstance(v, float) and not math.isfinite(v):
             result["plan_info"][k] = None

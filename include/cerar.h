@@ -98,6 +98,8 @@ typedef struct {
                              * permutations leave ||H||, D's spectrum and so Phi unchanged, but
                              * a small gamma makes the windows A_l, and so M_i, ill-conditioned. */
     int n_node_perms;       /* 0: H as above (perturb, else diag(nodes)); at most 4096 */
+    int svd_sweeps;         /* cap on the sweeps of each one-sided Jacobi SVD (the projection,
+                             * kappa, gamma and ||H||); 0 selects 80 */
 } cerar_plan_desc;
 
 /* Plan diagnostics (host fp64). */
@@ -120,6 +122,10 @@ typedef struct {
     double gamma;                 /* O_EPS, KAPPA: min_l sigma_min(K^(l)(B, H)) of the (B, H) used
                                    * (Sec. II-C assumption); NaN otherwise */
     int h_choice;                 /* index of the chosen node permutation, -1 if none was given */
+    int svd_converged;            /* 1 when every one-sided Jacobi SVD behind kappa_M, kappa_U,
+                                   * kappa_R, amplification, gamma and ||H||_2 converged within the
+                                   * sweep cap; 0 when one stopped at the cap (those figures are
+                                   * then approximate) */
 } cerar_plan_info;
 
 /* Build a plan on the host in fp64 (Sec. II-B to II-D): B and D (or the
@@ -128,8 +134,10 @@ typedef struct {
  * of Sec. II-D from the O(eps0) plan.  Synchronous; touches no device.
  * Errors: E_INVAL (N < 2, N > 64, c < N, c > 128, param out of range,
  * node_perms with perturb, with VANDERMONDE or not permutations,
- * out == NULL), E_SINGULAR (a window A_l exactly singular for 8 seeds, or for
- * the given B), E_NOMEM. */
+ * svd_sweeps < 0, out == NULL), E_SINGULAR (a window A_l exactly singular
+ * for 8 seeds, or for the given B), E_NOCONV (KAPPA: the SVD of an encoder
+ * in the projection did not converge within svd_sweeps, so the kappa bound
+ * would not be guaranteed), E_NOMEM. */
 int cerar_plan_create(int N, int c, cerar_construction kind, double param,
                       uint64_t seed, cerar_plan **out);
 int cerar_plan_create_desc(const cerar_plan_desc *desc, cerar_plan **out);
@@ -146,11 +154,11 @@ void cerar_plan_destroy(cerar_plan *plan);
 /* Uploads the plan's fp32 coefficient fragments and slot tables to the
  * current device, once per plan and device (hipMalloc and a synchronous
  * hipMemcpy); later calls for that device return at once.  Every enqueueing
- * call does this itself on its first use on a device.  Calling it first lets
- * a caller record those calls into a HIP graph by stream capture without an
- * eager call, since after it they issue kernel launches only.  Thread-safe.
- * Errors: E_INVAL (NULL plan); E_DEVICE (a HIP call failed; nothing is kept
- * for that device). */
+ * call does this itself on its first use on a device.  Calling it first
+ * lets a caller record the enqueueing calls into a HIP graph by stream
+ * capture without an eager call, since after it they issue kernel launches
+ * only.  Thread-safe.  Errors: E_INVAL (NULL plan); E_DEVICE (a HIP call
+ * failed; nothing is kept for that device). */
 int cerar_plan_prepare_device(const cerar_plan *plan);
 
 int cerar_plan_get_info(const cerar_plan *plan, cerar_plan_info *info);
@@ -254,7 +262,8 @@ int cerar_ring_simulate_fused(const cerar_plan *plan, size_t d, const float *gra
  * Errors: E_INVAL (NULL plan or buffers, nbuckets < 1, an empty bucket,
  * overlapping buckets, ld_work below the slot total, ld_grads or ld_out below
  * the largest bucket end, out overlapping work or ws, grads overlapping
- * work, or a bucket too long for one launch); E_DEVICE. */
+ * work or ws, work overlapping ws, or a bucket too long for one launch);
+ * E_DEVICE. */
 int cerar_bucketed_workspace_bytes(const cerar_plan *plan, const size_t *bucket_len,
                                    int nbuckets, size_t *work_floats, size_t *ws_bytes);
 int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,
@@ -277,6 +286,24 @@ int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_grads,
  * scales the HBM traffic counters.  n == 0 does nothing.  Errors: E_INVAL
  * (NULL or overlapping buffers, a copy too long for one launch); E_DEVICE. */
 int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stream stream);
+
+/* Measurement and test input (not part of the method): the seeded
+ * synthetic gradient entries of the benchmark workloads, generated on the
+ * device.  out[t] (device, n floats) = entry first + t of the stream `key`:
+ * the Irwin-Hall sum of twelve 32-bit halves of splitmix64 hashes of
+ * key + (8 idx + slot + 1) * 0x9E3779B97F4A7C15 (slots 0..5) minus 6, times
+ * outlier_factor when the low half of slot 6 is below outlier_threshold (0:
+ * never), times the scale of the tensor that holds idx (one fp64 product),
+ * rounded once to fp32; 0 for idx >= d (the zero pad).  Tensor j covers flat
+ * indices [tensor_off[j], tensor_off[j+1]); tensor_off (int64, ntensors + 1
+ * entries, ascending, tensor_off[0] = 0) and tensor_scale (fp32, ntensors)
+ * are device arrays owned by the caller.  The host generator of the tests
+ * computes the same function, so both give identical bits.  n == 0 does
+ * nothing.  Errors: E_INVAL (NULL pointers, ntensors outside [1, 1024],
+ * first + n beyond 2^64); E_DEVICE. */
+int cerar_synth_fill(float *out, size_t n, uint64_t first, uint64_t d, uint64_t key,
+                     const int64_t *tensor_off, const float *tensor_scale, int ntensors,
+                     uint32_t outlier_threshold, double outlier_factor, cerar_stream stream);
 
 /* Text of the calling thread's last non-OK status ("" if none). */
 const char *cerar_last_error(void);

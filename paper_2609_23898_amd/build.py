@@ -12,7 +12,7 @@ OUT = os.path.join(HERE, "libcerar.so")
 EXAMPLE_SRC = os.path.join(ROOT, "tests", "c_abi", "allreduce.c")
 EXAMPLE = os.path.join(ROOT, "tests", "c_abi", "allreduce")
 
-HIP_SOURCES = ["kernels.hip"]
+HIP_SOURCES = ["kernels.hip", "synth.hip"]
 CXX_SOURCES = ["plan.cpp", "linalg.cpp"]
 
 # Packed fp32 instructions stay disabled in every HIP translation unit.

@@ -35,7 +35,8 @@ class PlanDesc(ctypes.Structure):
                 ("perturb", ctypes.POINTER(ctypes.c_double)),
                 ("nodes", ctypes.POINTER(ctypes.c_double)),
                 ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int), ("als_order", ctypes.c_int),
-                ("node_perms", ctypes.POINTER(ctypes.c_int)), ("n_node_perms", ctypes.c_int)]
+                ("node_perms", ctypes.POINTER(ctypes.c_int)), ("n_node_perms", ctypes.c_int),
+                ("svd_sweeps", ctypes.c_int)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -47,7 +48,8 @@ class PlanInfo(ctypes.Structure):
                 ("amplification", ctypes.c_double), ("comm_rate", ctypes.c_double),
                 ("storage_rate", ctypes.c_double), ("proj_a0", ctypes.c_double),
                 ("proj_b0", ctypes.c_double), ("fp64_reliable", ctypes.c_int),
-                ("seed_used", ctypes.c_uint64), ("gamma", ctypes.c_double), ("h_choice", ctypes.c_int)]
+                ("seed_used", ctypes.c_uint64), ("gamma", ctypes.c_double), ("h_choice", ctypes.c_int),
+                ("svd_converged", ctypes.c_int)]
 
 
 _P = ctypes.c_void_p
@@ -76,6 +78,8 @@ SIGNATURES = {
                                           _P, _P, _SZ, _P]),
     "cerar_error_norms": (_I, [_I, _SZ, _P, _SZ, _P, _SZ, _P, _P]),
     "cerar_copy_f32": (_I, [_P, _P, _SZ, _P]),
+    "cerar_synth_fill": (_I, [_P, _SZ, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, _P, _P, _I,
+                              ctypes.c_uint32, ctypes.c_double, _P]),
     "cerar_last_error": (ctypes.c_char_p, []),
 }
 
@@ -134,7 +138,7 @@ class Plan:
     """Encoding/decoding plan (host fp64), see cerar_plan_create_desc."""
 
     def __init__(self, N, c, kind, param=0.0, seed=0, base=None, perturb=None, nodes=None,
-                 eps0=0.0, als_iters=0, als_order=0, node_perms=None, _handle=None):
+                 eps0=0.0, als_iters=0, als_order=0, node_perms=None, svd_sweeps=0, _handle=None):
         L = lib()
         self._h = _P()
         if _handle is not None:
@@ -159,7 +163,7 @@ class Plan:
                 perms, nperm = pa.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), pa.shape[0]
             desc = PlanDesc(N, c, kind, float(param), int(seed), arr(base, N * c),
                             arr(perturb, c * c), arr(nodes, c), float(eps0), int(als_iters),
-                            int(als_order), perms, nperm)
+                            int(als_order), perms, nperm, int(svd_sweeps))
             _check(L.cerar_plan_create_desc(ctypes.byref(desc), ctypes.byref(self._h)))
         info = self.info()
         self.N, self.c, self.L = info["N"], info["c"], info["L"]
@@ -372,6 +376,36 @@ def copy_f32(dst, src, stream=None):
     if dst.numel() != src.numel():
         raise ValueError(f"dst has {dst.numel()} elements, src {src.numel()}")
     _check(lib().cerar_copy_f32(_ptr(dst), _ptr(src), dst.numel(), _stream(stream)))
+
+
+_SYNTH_TABLES = {}
+
+
+def _synth_tables(wl, device):
+    """Device copies of a workload's tensor offsets and scales (cached)."""
+    import torch
+    k = (id(wl), str(device))
+    if k not in _SYNTH_TABLES:
+        offs = torch.as_tensor(np.ascontiguousarray(wl._offsets, dtype=np.int64), device=device)
+        scales = torch.as_tensor(np.ascontiguousarray(wl._scales, dtype=np.float32), device=device)
+        _SYNTH_TABLES[k] = (wl, offs, scales)
+    return _SYNTH_TABLES[k][1:]
+
+
+def synth_fill(out, wl, worker, start=0, stream=None):
+    """Entries [start, start + out.numel()) of the workload's gradient of
+    `worker` into the contiguous float32 device tensor `out`, generated by
+    the library's K6 kernel (cerar_synth_fill); the same bits as
+    wl.values_np(worker, indices)."""
+    _on_device(out, "out")
+    if str(out.dtype) != "torch.float32" or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor")
+    offs, scales = _synth_tables(wl, out.device)
+    thr = wl.outlier_threshold if wl.outlier_prob > 0 else 0
+    _check(lib().cerar_synth_fill(_ptr(out), out.numel(), int(start), int(wl.d), int(wl.worker_key(worker)),
+                                  _ptr(offs), _ptr(scales), int(scales.numel()), int(thr),
+                                  float(wl.outlier_factor), _stream(stream)))
+    return out
 
 
 def algorithmic_bytes_per_worker(N, c, p):

@@ -66,6 +66,8 @@ struct cerar_plan {
     std::vector<double> U;           // N x c x c: U[k][l][j]
     std::vector<double> R;           // N x (L+1) x c: R[i][k][m]
     std::vector<double> B, D;        // MPC base / perturbation (empty for EXPLICIT)
+    int svd_sweeps = 80;             // cap on one-sided Jacobi sweeps per SVD (cerar_plan_desc.svd_sweeps)
+    bool svd_ok = true;              // every SVD so far converged within svd_sweeps
     cerar::RingTables tab;
     int MT = 0, KSe = 0, KSd = 0;    // M-tiles, encode K-steps, decode K-steps
     std::vector<float> enc_frag, dec_frag;

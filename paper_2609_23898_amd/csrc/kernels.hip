@@ -639,6 +639,18 @@ constexpr int kRoundThreads = 256;
 
 // One workgroup's share of a round for one worker: positions
 // [wg, wg + 1) x 1024 (vector layout) or a grid-stride loop (scalar layout).
+// The next message of a round N <= k < c, x = recv - delta_j + delta_{k+1},
+// rounded to fp32 once: the three fp32 terms are combined in fp64 (the
+// difference of two fp32 values is exact there unless their exponents are
+// more than 29 apart), so a message carries one rounding per round instead
+// of two.  A message keeps the rounding error of every earlier round (the
+// returning own term cancels, its rounding does not), and the decode
+// amplifies those errors by up to kappa_2(M_i), so this is the round's
+// share of the final error.
+__device__ inline float combine3(float recv, float sub, float add) {
+    return (float)(((double)recv - (double)sub) + (double)add);
+}
+
 template <int MODE, bool VEC>
 __device__ inline void round_body(const SlotBase &sb, const RoundOp &op, unsigned wg, unsigned wgpw) {
     const float *recv = sb.ptr(op.recv);
@@ -650,15 +662,21 @@ __device__ inline void round_body(const SlotBase &sb, const RoundOp &op, unsigne
         const size_t i = ((size_t)wg * kRoundThreads + threadIdx.x) * 4;
         if (i < p) {
             v4f v = nt_load(recv + i);
-            if (MODE >= 1) v = v - nt_load(sub + i);
-            if (MODE <= 1) v = v + nt_load(add + i);
+            if (MODE == 0) v = v + nt_load(add + i);
+            if (MODE == 2) v = v - nt_load(sub + i);
+            if (MODE == 1) {
+                const v4f s = nt_load(sub + i), t = nt_load(add + i);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[q] = combine3(v[q], s[q], t[q]);
+            }
             nt_store(dst + i, v);
         }
     } else {
         for (size_t i = (size_t)wg * kRoundThreads + threadIdx.x; i < p; i += (size_t)wgpw * kRoundThreads) {
             float v = recv[i];
-            if (MODE >= 1) v = v - sub[i];
-            if (MODE <= 1) v = v + add[i];
+            if (MODE == 0) v = v + add[i];
+            if (MODE == 2) v = v - sub[i];
+            if (MODE == 1) v = combine3(v, sub[i], add[i]);
             dst[i] = v;
         }
     }
@@ -1165,8 +1183,9 @@ __global__ __launch_bounds__(MAXT) void k_fused(FusedParams a) {
                     x = recv + mydelta[(size_t)k * 64 + lane];                   // + delta_{w,k+1}
                 } else {
                     const int j = k - N + 1;
-                    x = recv - mydelta[(size_t)(j - 1) * 64 + lane];             // - delta_{w,j}
-                    if (k + 1 <= C) x += mydelta[(size_t)k * 64 + lane];         // + delta_{w,k+1}
+                    const float sub = mydelta[(size_t)(j - 1) * 64 + lane];      // - delta_{w,j}
+                    x = k + 1 <= C ? combine3(recv, sub, mydelta[(size_t)k * 64 + lane])   // + delta_{w,k+1}
+                                   : recv - sub;
                 }
                 msg[(size_t)(k & 1) * N * 64 + (size_t)w * 64 + lane] = x;
             }
@@ -1278,9 +1297,10 @@ __global__ __launch_bounds__(64 * NW) void k_fused_lanes(FusedParams a) {
             if (k < L) {
                 if (k <= NW - 1) {
                     x = recv + dl[k];                    // + delta_{rw,k+1}
+                } else if (k + 1 <= C) {
+                    x = combine3(recv, dl[k - NW], dl[k]);   // - delta_{rw,k-N+1} + delta_{rw,k+1}
                 } else {
                     x = recv - dl[k - NW];               // - delta_{rw,k-N+1}
-                    if (k + 1 <= C) x += dl[k];          // + delta_{rw,k+1}
                 }
             }
         }
@@ -2342,6 +2362,9 @@ static int ring_simulate_bucketed_impl(const cerar_plan *plan, int nbuckets, con
         return fail(CERAR_E_INVAL, "out overlaps work or ws");
     if (overlap(grads, ((N - 1) * ld_grads + span) * sizeof(float), work, work_bytes))
         return fail(CERAR_E_INVAL, "bucketed encode is out of place: grads and work must not overlap");
+    if (overlap(work, work_bytes, ws, ws_bytes)) return fail(CERAR_E_INVAL, "work and ws overlap");
+    if (overlap(grads, ((N - 1) * ld_grads + span) * sizeof(float), ws, ws_bytes))
+        return fail(CERAR_E_INVAL, "grads and ws overlap");
     const DeviceCopy *dc;
     st = device_copy(plan, &dc);
     if (st) return st;

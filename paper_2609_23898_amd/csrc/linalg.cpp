@@ -153,14 +153,15 @@ bool lstsq(const double *A, int m, int n, const double *B, int k, double *X) {
 
 // One-sided Jacobi on the columns of the column-major m x n matrix W (m >= n).
 // Columns become mutually orthogonal; V (column-major n x n) accumulates the
-// rotations when non-null.
-static void jacobi_columns(double *W, int m, int n, double *V) {
+// rotations when non-null.  Returns false when a sweep still rotated after
+// max_sweeps sweeps (the columns are then not orthogonal to working accuracy).
+static bool jacobi_columns(double *W, int m, int n, double *V, int max_sweeps) {
     if (V) {
         std::fill(V, V + (size_t)n * n, 0.0);
         for (int i = 0; i < n; ++i) V[(size_t)i * n + i] = 1.0;
     }
     const double tol = 1e-15;
-    for (int sweep = 0; sweep < 80; ++sweep) {
+    for (int sweep = 0; sweep < max_sweeps; ++sweep) {
         bool rotated = false;
         for (int p = 0; p < n - 1; ++p) {
             for (int q = p + 1; q < n; ++q) {
@@ -192,11 +193,12 @@ static void jacobi_columns(double *W, int m, int n, double *V) {
                 }
             }
         }
-        if (!rotated) break;
+        if (!rotated) return true;
     }
+    return n < 2;
 }
 
-std::vector<double> singular_values(const double *A, int m, int n) {
+std::vector<double> singular_values(const double *A, int m, int n, int max_sweeps, bool *converged) {
     // Work on the taller orientation, column-major.
     const bool trans = m < n;
     const int mm = trans ? n : m, nn = trans ? m : n;
@@ -224,18 +226,19 @@ std::vector<double> singular_values(const double *A, int m, int n) {
                 }
         }
     }
-    jacobi_columns(W.data(), rows, nn, nullptr);
+    const bool ok = jacobi_columns(W.data(), rows, nn, nullptr, max_sweeps);
+    if (!ok && converged) *converged = false;
     std::vector<double> s(nn);
     for (int j = 0; j < nn; ++j) s[j] = std::sqrt(frobenius2(W.data() + (size_t)j * rows, rows));
     std::sort(s.begin(), s.end(), std::greater<double>());
     return s;
 }
 
-void svd_square(const double *A, int n, double *P, double *s, double *Q) {
+bool svd_square(const double *A, int n, double *P, double *s, double *Q, int max_sweeps) {
     Mat W((size_t)n * n), V((size_t)n * n);
     for (int i = 0; i < n; ++i)
         for (int j = 0; j < n; ++j) W[(size_t)j * n + i] = A[(size_t)i * n + j];
-    jacobi_columns(W.data(), n, n, V.data());
+    const bool converged = jacobi_columns(W.data(), n, n, V.data(), max_sweeps);
     std::vector<double> sig(n);
     for (int j = 0; j < n; ++j) sig[j] = std::sqrt(frobenius2(W.data() + (size_t)j * n, n));
     std::vector<int> order(n);
@@ -275,6 +278,7 @@ void svd_square(const double *A, int n, double *P, double *s, double *Q) {
     }
     for (int i = 0; i < n; ++i)
         for (int t = 0; t < n; ++t) P[(size_t)i * n + t] = Pc[(size_t)t * n + i];
+    return converged;
 }
 
 }  // namespace la

@@ -25,13 +25,20 @@ bool solve(const double *A, int n, double *B, int m);
 // full column rank, via Householder QR.  Returns false on rank deficiency.
 bool lstsq(const double *A, int m, int n, const double *B, int k, double *X);
 
+// Default cap on the sweeps of one-sided Jacobi.
+constexpr int kJacobiSweeps = 80;
+
 // Singular values of A (m x n), descending.  Tall inputs are reduced by QR
-// first, then one-sided Jacobi (Hestenes) runs on the small factor.
-std::vector<double> singular_values(const double *A, int m, int n);
+// first, then one-sided Jacobi (Hestenes) runs on the small factor.  When
+// converged is non-null, it is set to false if Jacobi reached max_sweeps
+// without converging (and left alone otherwise).
+std::vector<double> singular_values(const double *A, int m, int n, int max_sweeps = kJacobiSweeps,
+                                    bool *converged = nullptr);
 
 // Full SVD of a square n x n matrix: A = P diag(s) Q^T with s descending,
-// P and Q orthogonal (row-major n x n).  One-sided Jacobi.
-void svd_square(const double *A, int n, double *P, double *s, double *Q);
+// P and Q orthogonal (row-major n x n).  One-sided Jacobi.  Returns false if
+// it reached max_sweeps without converging.
+bool svd_square(const double *A, int n, double *P, double *s, double *Q, int max_sweeps = kJacobiSweeps);
 
 double frobenius2(const double *A, size_t count);
 

@@ -234,13 +234,18 @@ bool r_step(const cerar_plan *p, const std::vector<double> &U, std::vector<doubl
 
 // Clip every U_k's singular values into [a0, b0], b0/a0 = kappa_max/sqrt(N),
 // geometrically centred on the geometric mean of all singular values.
-void project(const cerar_plan *p, std::vector<double> &U, double kappa_max, double &a0, double &b0) {
+// Returns false when an SVD did not converge within the plan's sweep cap
+// (U is then left unchanged: the clipping would rest on inexact factors).
+bool project(const cerar_plan *p, std::vector<double> &U, double kappa_max, double &a0, double &b0) {
     const int N = p->N, c = p->c;
     std::vector<double> P((size_t)N * c * c), S((size_t)N * c), Q((size_t)N * c * c);
+    std::vector<char> ok(N, 1);
     parallel_for(N, [&](int k) {
-        la::svd_square(U.data() + (size_t)k * c * c, c, P.data() + (size_t)k * c * c,
-                       S.data() + (size_t)k * c, Q.data() + (size_t)k * c * c);
+        ok[k] = la::svd_square(U.data() + (size_t)k * c * c, c, P.data() + (size_t)k * c * c,
+                               S.data() + (size_t)k * c, Q.data() + (size_t)k * c * c, p->svd_sweeps);
     });
+    for (char v : ok)
+        if (!v) return false;
     double logsum = 0.0;
     for (double s : S) logsum += std::log(s);
     const double centre = std::exp(logsum / (double)S.size());
@@ -259,10 +264,11 @@ void project(const cerar_plan *p, std::vector<double> &U, double kappa_max, doub
                 Uk[(size_t)a * c + b] = v;
             }
     }
+    return true;
 }
 
-double kappa_of(const double *A, int m, int n) {
-    std::vector<double> s = la::singular_values(A, m, n);
+double kappa_of(const double *A, int m, int n, int sweeps, bool *converged) {
+    std::vector<double> s = la::singular_values(A, m, n, sweeps, converged);
     return s.back() > 0 ? s.front() / s.back() : std::numeric_limits<double>::infinity();
 }
 
@@ -279,16 +285,22 @@ void fill_info(cerar_plan *p, cerar_construction kind, double param) {
     I.storage_rate = 1.0 + (double)N / c;
     I.phi = phi_of(p, p->U, p->R);
     std::vector<double> kM(N), kU(N), kR(N), nU(N), nR(N);
+    std::vector<char> conv(N, 1);
     parallel_for(N, [&](int i) {
+        bool ok = true;
         std::vector<double> M = coefficient_map(p, p->U, i);
-        kM[i] = kappa_of(M.data(), N * c, L + 1);
-        std::vector<double> su = la::singular_values(p->U.data() + (size_t)i * c * c, c, c);
+        kM[i] = kappa_of(M.data(), N * c, L + 1, p->svd_sweeps, &ok);
+        std::vector<double> su = la::singular_values(p->U.data() + (size_t)i * c * c, c, c, p->svd_sweeps, &ok);
         kU[i] = su.back() > 0 ? su.front() / su.back() : INFINITY;
         nU[i] = su.front();
-        std::vector<double> sr = la::singular_values(p->R.data() + (size_t)i * (L + 1) * c, L + 1, c);
+        std::vector<double> sr = la::singular_values(p->R.data() + (size_t)i * (L + 1) * c, L + 1, c,
+                                                     p->svd_sweeps, &ok);
         kR[i] = sr.back() > 0 ? sr.front() / sr.back() : INFINITY;
         nR[i] = sr.front();
+        conv[i] = ok;
     });
+    for (char v : conv) p->svd_ok = p->svd_ok && v;
+    I.svd_converged = p->svd_ok ? 1 : 0;
     I.kappa_M = *std::max_element(kM.begin(), kM.end());
     I.kappa_U = *std::max_element(kU.begin(), kU.end());
     I.kappa_R = *std::max_element(kR.begin(), kR.end());
@@ -325,13 +337,18 @@ std::vector<double> k_matrix(const std::vector<double> &B, const std::vector<dou
 }
 
 // gamma = min over l of sigma_min(K^(l)(B, H)); with s = 0 every l gives the same K.
-double gamma_of(const std::vector<double> &B, const std::vector<double> &H, int N, int c) {
+// Clears p->svd_ok if an SVD reached the sweep cap.
+double gamma_of(cerar_plan *p, const std::vector<double> &B, const std::vector<double> &H, int N, int c) {
     const int nl = (c % N) ? N : 1;
     std::vector<double> g(nl);
+    std::vector<char> conv(nl, 1);
     parallel_for(nl, [&](int ell) {
+        bool ok = true;
         std::vector<double> K = k_matrix(B, H, N, c, ell);
-        g[ell] = la::singular_values(K.data(), c, c).back();
+        g[ell] = la::singular_values(K.data(), c, c, p->svd_sweeps, &ok).back();
+        conv[ell] = ok;
     });
+    for (char v : conv) p->svd_ok = p->svd_ok && v;
     return *std::min_element(g.begin(), g.end());
 }
 
@@ -357,6 +374,7 @@ int validate(const cerar_plan_desc *d) {
         default:
             return fail(CERAR_E_INVAL, "unknown construction %d", (int)d->kind);
     }
+    if (d->svd_sweeps < 0) return fail(CERAR_E_INVAL, "svd_sweeps=%d must be >= 0", d->svd_sweeps);
     if (d->n_node_perms < 0 || d->n_node_perms > kMaxNodePerms)
         return fail(CERAR_E_INVAL, "n_node_perms=%d outside [0, %d]", d->n_node_perms, kMaxNodePerms);
     if (d->n_node_perms > 0) {
@@ -543,6 +561,7 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
     p->info.proj_a0 = p->info.proj_b0 = kNaN;
     p->info.gamma = kNaN;
     p->info.h_choice = -1;
+    if (desc->svd_sweeps > 0) p->svd_sweeps = desc->svd_sweeps;
     int result = CERAR_OK;
     if (desc->kind == CERAR_VANDERMONDE) {
         // z_j = exp(tau xi_j); b_l = [z_j^l], l < N; D = diag(z_j^N)
@@ -557,7 +576,9 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
     } else {
         const double eps = desc->kind == CERAR_O_EPS ? desc->param : (desc->eps0 > 0 ? desc->eps0 : 0.3);
         if (desc->kind == CERAR_O_EPS && eps > 0) {
-            std::vector<double> s = la::singular_values(H.data(), c, c);
+            bool ok = true;
+            std::vector<double> s = la::singular_values(H.data(), c, c, p->svd_sweeps, &ok);
+            p->svd_ok = p->svd_ok && ok;
             if (eps * s.front() >= 1.0)
                 return fail(CERAR_E_INVAL, "eps ||H||_2 = %g must be < 1 (Sec. II-C)", eps * s.front());
         }
@@ -577,7 +598,7 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
                 for (int q = 0; q < desc->n_node_perms; ++q) {
                     const int *perm = desc->node_perms + (size_t)q * c;
                     for (int j = 0; j < c; ++j) Ht[(size_t)j * c + j] = nodes[perm[j]];
-                    const double g = gamma_of(p->B, Ht, N, c);
+                    const double g = gamma_of(p, p->B, Ht, N, c);
                     if (g > best) {
                         best = g;
                         H = Ht;
@@ -586,7 +607,7 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
                 }
                 p->info.gamma = best;
             } else {
-                p->info.gamma = gamma_of(p->B, H, N, c);
+                p->info.gamma = gamma_of(p, p->B, H, N, c);
             }
             p->D.assign((size_t)c * c, 0.0);
             for (size_t a = 0; a < H.size(); ++a) p->D[a] = eps * H[a];
@@ -599,15 +620,22 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
             const int iters = desc->als_iters > 0 ? desc->als_iters : 100;
             double a0 = kNaN, b0 = kNaN;
             const bool project_first = desc->als_order == 1;
+            // the kappa guarantee rests on the projection's SVDs: one that
+            // did not converge fails the plan instead of weakening it
+            auto no_conv = [&] {
+                return fail(CERAR_E_NOCONV, "one-sided Jacobi SVD of an encoder did not converge in %d sweeps "
+                            "(projection of Sec. II-D)", p->svd_sweeps);
+            };
             for (int it = 0; it < iters && result == CERAR_OK; ++it) {
                 if (!u_step(p, p->R, p->U)) {
                     result = fail(CERAR_E_SINGULAR, "U-step normal equations singular");
                 } else if (project_first) {             // U-step, projection, R-step
-                    project(p, p->U, desc->param, a0, b0);
-                    if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
+                    if (!project(p, p->U, desc->param, a0, b0)) result = no_conv();
+                    else if (!r_step(p, p->U, p->R))
+                        result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
                 } else {                                // U-step, R-step, projection (Sec. II-D)
                     if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
-                    else project(p, p->U, desc->param, a0, b0);
+                    else if (!project(p, p->U, desc->param, a0, b0)) result = no_conv();
                 }
             }
             // the decoders of the final (projected) encoders

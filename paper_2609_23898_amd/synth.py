@@ -11,8 +11,9 @@ makes numbers.  Every value is a pure function of (seed, stream, index):
   as published with splitmix64) gives 64 random bits per counter;
 * an approximately standard normal value is the Irwin-Hall sum of twelve
   32-bit uniforms minus 6.  It is computed with exact integer arithmetic and
-  one exact scaling by 2^-32, so NumPy, torch on the CPU and torch on the GPU
-  all produce the same bits;
+  one exact scaling by 2^-32, so this NumPy path and the library's device
+  generator (cerar_synth_fill, which the device-side callers use) produce
+  the same bits;
 * a gradient entry is float32(normal * scale), where the scale comes from a
   per-tensor table computed once on the host.  Every path does the same
   single float64 product and the same single rounding to float32.
@@ -54,11 +55,6 @@ def stream_key(seed, stream):
     return _mix64_int(_mix64_int((seed * _GOLDEN + 1) & _MASK64) ^ ((stream * _MUL2) & _MASK64))
 
 
-def _signed(v):
-    v &= _MASK64
-    return v - (1 << 64) if v >= (1 << 63) else v
-
-
 # --- NumPy path (uint64 arithmetic wraps by definition) ---------------------
 
 def _mix64_np(z):
@@ -91,38 +87,6 @@ def uniform32_np(key, idx, j):
     """One 32-bit uniform integer per counter from hash slot j."""
     h = _hash_np(key, np.asarray(idx, dtype=np.int64), j)
     return (h & np.uint64(0xFFFFFFFF)).astype(np.int64)
-
-
-# --- torch path (int64 with explicit logical shifts) -------------------------
-
-def _srl(z, s):
-    return (z >> s) & ((1 << (64 - s)) - 1)
-
-
-def _mix64_torch(z):
-    z = (z ^ _srl(z, 30)) * _signed(_MUL1)
-    z = (z ^ _srl(z, 27)) * _signed(_MUL2)
-    return z ^ _srl(z, 31)
-
-
-def _hash_torch(key, idx, j):
-    ctr = idx * _HASHES_PER_ENTRY + (j + 1)
-    return _mix64_torch(ctr * _signed(_GOLDEN) + _signed(key))
-
-
-def normal_torch(key, idx):
-    """Same values as ``normal_np``; ``idx`` is an int64 torch tensor."""
-    import torch
-    total = torch.zeros_like(idx)
-    for j in range(6):
-        h = _hash_torch(key, idx, j)
-        total += h & 0xFFFFFFFF
-        total += _srl(h, 32)
-    return (total + (6 - 6 * (1 << 32))).to(torch.float64) * 2.0 ** -32
-
-
-def uniform32_torch(key, idx, j):
-    return _hash_torch(key, idx, j) & 0xFFFFFFFF
 
 
 # --- workloads ---------------------------------------------------------------
@@ -239,36 +203,6 @@ class Workload:
         s = self._scales[t].astype(np.float64)
         v = (n * s).astype(np.float32)
         return np.where(valid, v, np.float32(0.0))
-
-    def values_torch(self, worker, idx):
-        """Same values as ``values_np`` for an int64 torch tensor of flat
-        indices, on the tensor's device."""
-        import torch
-        dev = idx.device
-        key = self.worker_key(worker)
-        offsets = torch.as_tensor(self._offsets, device=dev)
-        scales = torch.as_tensor(self._scales.astype(np.float64), device=dev)
-        valid = idx < self.d
-        idx_c = torch.where(valid, idx, torch.zeros_like(idx))
-        n = normal_torch(key, idx_c)
-        if self.outlier_prob > 0:
-            hit = uniform32_torch(key, idx_c, 6) < self.outlier_threshold
-            n = torch.where(hit, n * float(self.outlier_factor), n)
-        t = torch.searchsorted(offsets, idx_c, right=True) - 1
-        v = (n * scales[t]).to(torch.float32)
-        return torch.where(valid, v, torch.zeros_like(v))
-
-    def fill_torch(self, out, worker, start=0, chunk=1 << 24):
-        """Write entries [start, start + out.numel()) of ``worker`` into the
-        float32 tensor ``out`` (any device), chunk by chunk."""
-        import torch
-        flat = out.view(-1)
-        count = flat.numel()
-        for lo in range(0, count, chunk):
-            hi = min(count, lo + chunk)
-            idx = torch.arange(start + lo, start + hi, dtype=torch.int64, device=out.device)
-            flat[lo:hi] = self.values_torch(worker, idx)
-        return out
 
 
 def base_matrix(seed, N, c):

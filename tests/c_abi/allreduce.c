@@ -1,6 +1,7 @@
 /* A C consumer of libcerar: one approximate all-reduce of N workers'
  * gradients on the current GPU through the C ABI and the HIP runtime alone,
- * with no Python.  Two plans:
+ * with no Python.  The inputs come from the library's seeded generator
+ * (cerar_synth_fill, Irwin-Hall normals in [-6, 6]).  Two plans:
  *  - exact (c = N, eps = 0, Sec. II-B): every output must be the sum of the
  *    N gradients up to fp32 rounding of the coefficients (1e-5 relative);
  *  - condition-number constrained (c > N, kappa_max = 1e3, Sec. II-D): an
@@ -8,6 +9,7 @@
  *    cerar_error_norms.
  * Exit status 0 and the line "c-abi example ok" on success. */
 #include <math.h>
+#include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
 
@@ -49,20 +51,35 @@ static int run(int N, int c, cerar_construction kind, double param, size_t d, do
     double *sum = malloc(d * sizeof(double));
     double *hn = malloc((size_t)(N + 1) * sizeof(double));
     if (!hg || !ho || !sum || !hn) return 1;
-    for (size_t i = 0; i < (size_t)N * d; ++i) hg[i] = (float)(sin(1e-3 * (double)i) + 0.25 * (double)(i % 7));
-    for (size_t e = 0; e < d; ++e) {
-        sum[e] = 0.0;
-        for (int w = 0; w < N; ++w) sum[e] += hg[(size_t)w * d + e];
-    }
-    float *grads, *work, *out;
+    float *grads, *work, *out, *scale;
     void *ws;
     double *norms;
+    int64_t *toff;
     HIP(hipMalloc((void **)&grads, (size_t)N * d * sizeof(float)));
     HIP(hipMalloc((void **)&work, (size_t)N * ld_work * sizeof(float)));
     HIP(hipMalloc(&ws, ws_bytes));
     HIP(hipMalloc((void **)&out, (size_t)N * d * sizeof(float)));
     HIP(hipMalloc((void **)&norms, (size_t)(N + 1) * sizeof(double)));
-    HIP(hipMemcpy(grads, hg, (size_t)N * d * sizeof(float), hipMemcpyHostToDevice));
+    /* inputs: the library's seeded generator, one tensor of scale 1, one stream per worker */
+    const int64_t h_off[2] = {0, (int64_t)d};
+    const float h_scale = 1.0f;
+    HIP(hipMalloc((void **)&toff, sizeof h_off));
+    HIP(hipMalloc((void **)&scale, sizeof h_scale));
+    HIP(hipMemcpy(toff, h_off, sizeof h_off, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(scale, &h_scale, sizeof h_scale, hipMemcpyHostToDevice));
+    for (int w = 0; w < N; ++w)
+        CER(cerar_synth_fill(grads + (size_t)w * d, d, 0, d, 0x5eed0000u + (uint64_t)w, toff, scale, 1, 0, 1.0, NULL));
+    HIP(hipMemcpy(hg, grads, (size_t)N * d * sizeof(float), hipMemcpyDeviceToHost));
+    for (size_t e = 0; e < d; ++e) {
+        sum[e] = 0.0;
+        for (int w = 0; w < N; ++w) sum[e] += hg[(size_t)w * d + e];
+    }
+    int finite_inputs = 1;
+    for (size_t i = 0; i < (size_t)N * d; ++i) finite_inputs &= isfinite(hg[i]) && fabsf(hg[i]) <= 6.0f;
+    if (!finite_inputs || sum[0] == 0.0) {
+        fprintf(stderr, "generated inputs out of range\n");
+        return 1;
+    }
     CER(cerar_ring_simulate(plan, d, grads, d, work, ld_work, ws, out, d, NULL));
     CER(cerar_error_norms(N, d, grads, d, out, d, norms, NULL));
     HIP(hipDeviceSynchronize());
@@ -86,6 +103,8 @@ static int run(int N, int c, cerar_construction kind, double param, size_t d, do
     HIP(hipFree(ws));
     HIP(hipFree(out));
     HIP(hipFree(norms));
+    HIP(hipFree(toff));
+    HIP(hipFree(scale));
     free(hg);
     free(ho);
     free(sum);

@@ -29,7 +29,7 @@ def header_functions():
 
 def test_library_exports_every_declared_function():
     names = header_functions()
-    assert len(names) == 19
+    assert len(names) == 20
     lib = C.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -269,6 +269,16 @@ def test_device_calls_validate_before_touching_the_device():
     assert lib.cerar_ring_simulate_bucketed(plan.handle, 2, offs, lens, fake, 1000, ctypes.c_void_p(0x40000000),
                                             1 << 20, ws, out, 1000, None) == -1
     assert b"overlap" in lib.cerar_last_error()
+    # bucketed: work overlapping ws, grads overlapping ws
+    offs = (ctypes.c_size_t * 2)(0, 200)
+    bwork = 0x40000000
+    assert lib.cerar_ring_simulate_bucketed(plan.handle, 2, offs, lens, fake, 1000, ctypes.c_void_p(bwork),
+                                            1 << 20, ctypes.c_void_p(bwork + 1024), out, 1000, None) == -1
+    assert b"work and ws overlap" in lib.cerar_last_error()
+    assert lib.cerar_ring_simulate_bucketed(plan.handle, 2, offs, lens, ctypes.c_void_p(0x5000000), 1000,
+                                            ctypes.c_void_p(bwork), 1 << 20, ctypes.c_void_p(0x5000000 + 512),
+                                            out, 1000, None) == -1
+    assert b"grads and ws overlap" in lib.cerar_last_error()
 
 
 def test_chunk_len_and_workspace():
@@ -335,3 +345,34 @@ def test_binding_refuses_host_tensors():
                  lambda: C.copy_f32(out, g)):
         with pytest.raises(ValueError, match="must be a tensor on the GPU"):
             call()
+
+
+def test_jacobi_sweep_cap_is_reported():
+    """One-sided Jacobi that stops at its sweep cap is never silent: the
+    kappa design fails with E_NOCONV (its kappa bound rests on the
+    projection's SVDs, Sec. II-D), and every other plan reports
+    svd_converged = 0 (its kappa and gamma figures are then approximate)."""
+    ok = C.Plan(8, 32, "o_eps", 0.1, seed=3)
+    assert ok.info()["svd_converged"] == 1
+    capped = C.Plan(8, 32, "o_eps", 0.1, seed=3, svd_sweeps=1)
+    assert capped.info()["svd_converged"] == 0
+    U, R = ok.matrices()
+    np.testing.assert_array_equal(capped.matrices()[0], U)      # the plan itself does not depend on the SVDs
+    with pytest.raises(C.CerarError) as ei:
+        C.Plan(8, 32, "kappa", 1e3, seed=3, als_iters=2, svd_sweeps=1)
+    assert ei.value.status == -4 and "did not converge" in str(ei.value)
+    assert C.Plan(8, 32, "kappa", 1e3, seed=3, als_iters=2).info()["svd_converged"] == 1
+    with pytest.raises(C.CerarError) as ei:
+        C.Plan(8, 32, "o_eps", 0.1, seed=3, svd_sweeps=-1)
+    assert ei.value.status == -1
+
+
+@pytest.mark.parametrize("N,c,kind,param", [(4, 4, "vandermonde", 0.5), (4, 8, "vandermonde", 0.125),
+                                            (8, 16, "o_eps", 1e-3), (8, 64, "kappa", 1e3),
+                                            (16, 128, "o_eps", 1e-2)])
+def test_default_sweep_cap_suffices_for_the_workload_plans(N, c, kind, param):
+    """The workloads' plans (and the ill-conditioned ones among them) get
+    converged SVDs at the default cap."""
+    kw = {"als_iters": 3} if kind == "kappa" else {}
+    plan = C.Plan(N, c, kind, param, seed=1000 + N, **kw)
+    assert plan.info()["svd_converged"] == 1

@@ -115,7 +115,7 @@ def test_trace_summary_compares_trace_and_event_averages(tmp_path):
     trace_avg, event_avg, ratio = (float(x) for x in rows[0].split()[-3:])
     assert trace_avg == pytest.approx(0.45) and event_avg == pytest.approx(0.459)
     assert ratio == pytest.approx(0.459 / 0.45, abs=1e-3)
-    assert "other kernels (torch input generation, untimed)" in out.read_text()
+    assert "other kernels (input generation, torch copies; untimed)" in out.read_text()
 
 
 def test_more_than_one_gpu_is_refused():

@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 
 def test_bench_line_on_the_tiny_workload():
     run = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "tiny-n4-c4",
-                          "--steps", "3", "--warmup", "1", "--cpu-positions", "256", "--copy-floats", "65536"],
+                          "--steps", "3", "--warmup", "1", "--cpu-positions", "256", "--cpu-seconds", "1", "--copy-floats", "65536"],
                          capture_output=True, text=True, timeout=300)
     assert run.returncode == 0, run.stderr[-3000:]
     lines = [l for l in run.stdout.splitlines() if l.startswith("{")]
@@ -36,6 +36,11 @@ def test_bench_line_on_the_tiny_workload():
     assert r["traffic"] is None                     # the counter summary covers the headline only
     cb = b["cpu_baseline"]
     assert cb["kind"] == "oracle" and cb["cores"] >= 1 and cb["value"] > 0 and cb["sample"]
+    assert 1 <= cb["threads"] <= min(cb["cores"], 15) and "GPU line's plan" in cb["plan"]
+    ip = b["in_place_encode"]
+    assert ip["ms_per_step_events"]["median"] > 0 and ip["encode_ms"]["median"] > 0
+    sp = b["encode_spread"]
+    assert 0 < sp["min_ms"] <= sp["max_ms"] and "fresh_buffer" in sp
     # the tiny workload's Vandermonde plan (tau = 0.5, Sec. II-B) is a poor
     # approximation by construction (Phi about 185), so only finiteness is checked
     assert math.isfinite(b["approx_rel_err_max"])

@@ -119,7 +119,9 @@ CASES = [
     ("N8-c32", 8, 32, 32 * 2048, "kappa", 1e3),
     ("N8-c64-ragged", 8, 64, 64 * 1536 + 61, "kappa", 1e3),
     ("N13-c64", 13, 64, 64 * 900 + 29, "kappa", 1e3),      # K = 76: the 20-K-step decode
-    ("N2-c64", 2, 64, 64 * 700, "kappa", 5e2),             # K = 65: 17 K-steps padded to 18
+    ("N2-c64", 2, 64, 64 * 700, "kappa", 1e3),             # K = 65: 17 K-steps padded to 18; kappa_M = 953,
+                                                           # the top of the gated range
+    ("N2-c64-k500", 2, 64, 64 * 700 + 19, "kappa", 5e2),
     ("N16-c128", 16, 128, 128 * 320, "kappa", 1e3),
 ]
 
@@ -329,21 +331,39 @@ def test_host_threads_share_one_fresh_plan():
         assert bool(torch.equal(bufs[t][2], out)), t
 
 
-def test_in_place_encode_matches_out_of_place():
-    N, c, d = 4, 16, 16 * 1000
-    U, R = mpc_plan(N, c, 0.3, seed=9)
+IN_PLACE = [
+    # name, N, c, d, extra floats of row stride (odd: the scalar layout)
+    ("c16", 4, 16, 16 * 1000, 0),              # the pipelined encode
+    ("c5-ragged", 3, 5, 5 * 333 + 2, 0),       # c not a multiple of 16: the masked kernels
+    ("c64-ragged", 8, 64, 64 * 1536 + 61, 0),  # the double-buffered c = 64 encode, then the tail
+    ("c128-ragged", 4, 128, 128 * 320 + 7, 0), # the wide c = 128 encode, then the generic tail
+    ("c64-scalar", 4, 64, 64 * 500 + 3, 1),    # misaligned rows: the scalar layout
+]
+
+
+@pytest.mark.parametrize("name,N,c,d,extra", IN_PLACE, ids=[x[0] for x in IN_PLACE])
+def test_in_place_encode_matches_out_of_place(name, N, c, d, extra):
+    """work == grads (the storage rule of Sec. II: Delta_i overwrites G_i):
+    every kernel family reads a block's c input rows before it writes any of
+    them, so the result is bit-identical to the out-of-place encode."""
+    U, R = mpc_plan(N, c, 0.3, seed=9) if c <= 16 else orthogonal_plan(N, c, seed=9)
     plan = C.Plan.explicit(U, R)
     g = host_grads(N, d, seed=9)
     p, _ = plan.chunk_len(d)
     torch, dev = torch_dev()
-    a = to_device(np.pad(g, ((0, 0), (0, c * p - d))), ld=c * p)   # grads with room for c*p
-    work, ws, out = buffers(plan, d)
+    ld = c * p + extra
+    a = to_device(np.pad(g, ((0, 0), (0, c * p - d))), ld=ld)      # grads with room for c*p
+    work, ws, out = buffers(plan, d, ld_work=ld)
     C.ring_simulate(plan, d, a, work, ws, out)
     ws2 = torch.zeros_like(ws)
     out2 = torch.empty_like(out)
     C.ring_simulate(plan, d, a, a, ws2, out2)                        # encode in place
     sync()
     np.testing.assert_array_equal(out.cpu().numpy(), out2.cpu().numpy())
+    # the rows now hold the encoded chunks: the same bits as the separate work buffer
+    np.testing.assert_array_equal(a[:, :c * p].cpu().numpy(), work[:, :c * p].cpu().numpy())
+    ref = oracle_allreduce(g, U, R)
+    assert max_rel_l2(out2.double().cpu().numpy(), ref) <= gate(OP.max_kappa_M(U))
 
 
 def test_scalar_layout_matches_vector_layout():

@@ -9,8 +9,9 @@ mixes the L+1 observations at e), so the oracle's output at a sampled
 position is exactly the protocol's output there.
 
 Inputs on both sides come from the shared seeded generator: the device fills
-its buffers with it, the oracle evaluates it on the host at the sampled flat
-indices, and one check confirms the two agree bit for bit.  Plans come from
+its buffers with the library's K6 kernel (cerar_synth_fill), the oracle
+evaluates the NumPy generator on the host at the sampled flat indices, and
+one check confirms the two agree bit for bit.  Plans come from
 the oracle and enter the library through cerar_plan_create_explicit."""
 
 import numpy as np
@@ -21,7 +22,7 @@ from oracle import ring as OR
 from paper_2609_23898_amd import cerar as C
 from paper_2609_23898_amd import synth
 
-from gpu_util import CHUNK_ALIGN, gate, orthogonal_plan, torch_dev
+from gpu_util import CHUNK_ALIGN, U32, gate, orthogonal_plan, torch_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -73,9 +74,11 @@ def run_stepwise(plan, d, grads, work, ws, out):
 
 
 def device_grads(wl, torch, dev):
+    """The workload's gradients, generated on the device by the library's
+    K6 kernel (cerar_synth_fill)."""
     grads = torch.empty((wl.N, wl.d), dtype=torch.float32, device=dev)
     for w in range(wl.N):
-        wl.fill_torch(grads[w], w)
+        C.synth_fill(grads[w], wl, w)
     return grads
 
 
@@ -117,24 +120,101 @@ def _return_device_memory():
     torch.cuda.empty_cache()
 
 
+def slot_values(plan, d, work, ws, slots, pos):
+    """Host float64 values of the given slots at positions pos: S x len(slots)."""
+    torch, dev = torch_dev()
+    p, stride = plan.chunk_len(d)
+    Nc = plan.N * plan.c
+    wsf = ws.view(torch.float32)
+    pidx = torch.from_numpy(np.ascontiguousarray(pos, dtype=np.int64)).to(dev)
+    cols = []
+    for s in slots:
+        if s < Nc:
+            w, l = divmod(int(s), plan.c)
+            cols.append(work[w, l * p:(l + 1) * p][pidx])
+        else:
+            q = int(s) - Nc
+            cols.append(wsf[q * stride:q * stride + p][pidx])
+    return torch.stack(cols, dim=1).double().cpu().numpy()
+
+
+def check_stages(name, wl, U, R, plan, grads, work, ws, out, pos):
+    """Stage-by-stage checks that pin the kernels' arithmetic whatever the
+    plan's conditioning: the encode against the oracle's encode of the same
+    inputs, within the bound of an fp32 dot product of length c with
+    fp32-rounded coefficients, |err| <= (c + 4) u (|G| |U|); then the decode
+    applied to the device's own observations after round L against the
+    oracle's decode of those observations, |err| <= (K + 4) u (|Y| |R|),
+    K = L + 1 (Sec. II: Delta_i = G_i U_i; Sec. II-A: g_hat_i = Y_i R_i)."""
+    N, c, d = wl.N, wl.c, wl.d
+    p = OR.chunk_len(d, c, CHUNK_ALIGN)
+    G, flat, valid = host_inputs(wl, pos, c)
+    C.encode_round(plan, 0, d, grads, work, ws)
+    sync()
+    enc_ratio = 0.0
+    for i in range(N):
+        got = slot_values(plan, d, work, ws, [i * c + j for j in range(c)], pos)
+        exact = OR.encode(G[i], U[i])
+        bound = (c + 4) * U32 * (np.abs(G[i]) @ np.abs(U[i])) + 1e-38
+        assert np.all(np.abs(got - exact) <= bound), (name, "encode", i)
+        enc_ratio = max(enc_ratio, float(np.max(np.abs(got - exact) / bound)))
+    for k in range(1, plan.L + 1):
+        C.encode_round(plan, k, d, grads, work, ws)
+    C.decode(plan, d, work, ws, out)
+    sync()
+    sm = plan.slot_map(plan.L)
+    K = plan.L + 1
+    dec_ratio = 0.0
+    for i in range(N):
+        ycols = [sm[i, c + j] for j in range(N - 1)] + [sm[i, j] for j in range(c)]   # [B_1..B_{N-1} | D_1..D_c]
+        Y = slot_values(plan, d, work, ws, ycols, pos)
+        exact = OR.decode(Y, R[i])
+        bound = (K + 4) * U32 * (np.abs(Y) @ np.abs(R[i])) + 1e-38
+        got = gather(out[i:i + 1], flat[valid])[0]
+        diff = np.abs(got - exact[valid])
+        assert np.all(diff <= bound[valid]), (name, "decode", i)
+        dec_ratio = max(dec_ratio, float(np.max(diff / bound[valid])))
+    print(f"{name}: stages within bound on {len(pos)} positions: encode max err/bound {enc_ratio:.3g}, "
+          f"decode of the device's observations max err/bound {dec_ratio:.3g}", flush=True)
+
+
+def sync():
+    import torch
+    torch.cuda.synchronize()
+
+
 def test_iid_n8_c16_o_eps():
-    """N=8, c=16, d=2^24, O(eps=1e-3): a quarter of the positions (2^18 of
-    2^20); kappa(M) ~ 4e5, so parity is held to the kappa-scaled bound."""
+    """N=8, c=16, d=2^24.  A well-conditioned plan (orthogonal U_k,
+    least-squares R_i) is gated at 1e-4 on a quarter of the positions (2^18 of
+    2^20).  The workload's own O(eps=1e-3) plan (kappa_2(M) ~ 3e4) is held to
+    the kappa-scaled bound, and its encode and decode are each checked within
+    their fp32 dot-product bounds."""
     torch, dev = torch_dev()
     wl = synth.workload("iid-n8-c16-16m")
+    grads = device_grads(wl, torch, dev)
+    p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
+    pos = sample_positions(p, 1 << 18, 2)
+    # gated: orthogonal plan at the full shape
+    U, R = orthogonal_plan(wl.N, wl.c, seed=22)
+    kappa = OP.max_kappa_M(U)
+    assert kappa <= 1e3
+    plan = C.Plan.explicit(U, R)
+    work, ws, out = C.allocate(plan, wl.d, dev)
+    run_stepwise(plan, wl.d, grads, work, ws, out)
+    torch.cuda.synchronize()
+    check_sampled("iid-n8-c16-16m orthogonal plan", wl, U, R, grads, out, pos, kappa)
+    plan.close()
+    # the workload's O(eps) plan
     B = synth.base_matrix(1000 + wl.N, wl.N, wl.c)
     U, R = OP.mpc_plan(B, OP.o_eps_perturbation(np.diag(OP.chebyshev_nodes(wl.c)), 1e-3))
     kappa = OP.max_kappa_M(U)
     plan = C.Plan.explicit(U, R)
-    grads = device_grads(wl, torch, dev)
-    work, ws, out = C.allocate(plan, wl.d, dev)
     run_stepwise(plan, wl.d, grads, work, ws, out)
     torch.cuda.synchronize()
-    p = OR.chunk_len(wl.d, wl.c, CHUNK_ALIGN)
-    parity, err_gpu, err_orc = check_sampled("iid-n8-c16-16m", wl, U, R, grads, out,
-                                             sample_positions(p, 1 << 18, 2), kappa)
+    parity, err_gpu, err_orc = check_sampled("iid-n8-c16-16m O(eps=1e-3)", wl, U, R, grads, out, pos, kappa)
     # the O(eps) error is the plan's, not the arithmetic's: eq. (14) bounds Phi
     assert err_orc < 1e-2
+    check_stages("iid-n8-c16-16m O(eps=1e-3)", wl, U, R, plan, grads, work, ws, out, pos[::16])
 
 
 def test_gpt2_small_buckets():
@@ -218,6 +298,8 @@ def test_heavy_tail_n16_c128():
           f"closed form: gpu {dev_gpu:.3g}, fp64 oracle {dev_orc:.3g}; closed-form error vs the "
           f"exact sum {err_closed:.4g}", flush=True)
     assert err_closed < 0.1                            # the plan itself is accurate (Prop. 2)
+    # the kernels' arithmetic on this plan, stage by stage, whatever its conditioning
+    check_stages("heavytail-n16-c128 O(eps=1e-2)", wl, U, R, plan, grads, work, ws, out, pos[::4])
 
 
 def test_chunks_longer_than_the_fast_path_offsets():

@@ -1,6 +1,7 @@
-"""The seeded input generators: the published splitmix64 sequence, identical
-bits on the NumPy and torch paths, the distributions the workloads ask for,
-and the model shapes and bucket layout of the synthetic gradients."""
+"""The seeded input generators: the published splitmix64 sequence, the NumPy
+path against the generator's definition in Python integers, the
+distributions the workloads ask for, and the model shapes and bucket layout
+of the synthetic gradients."""
 
 import math
 
@@ -22,33 +23,42 @@ def test_splitmix64_matches_published_sequence():
                    4593380528125082431, 16408922859458223821]
 
 
-def test_numpy_and_torch_paths_give_identical_bits():
-    torch = pytest.importorskip("torch")
+def _value_python(wl, worker, idx):
+    """One entry from Python integers and floats alone: the definition of the
+    generator written out, independent of the NumPy vectorisation."""
+    import bisect
+    if idx >= wl.d:
+        return np.float32(0.0)
+    key = wl.worker_key(worker)
+
+    def bits(slot):
+        return synth._mix64_int((key + (idx * 8 + slot + 1) * synth._GOLDEN) & synth._MASK64)
+
+    total = sum((h & 0xFFFFFFFF) + (h >> 32) for h in (bits(j) for j in range(6)))
+    v = float(total + 6 - 6 * (1 << 32)) * 2.0 ** -32
+    if wl.outlier_prob > 0 and (bits(6) & 0xFFFFFFFF) < wl.outlier_threshold:
+        v = v * float(wl.outlier_factor)
+    t = bisect.bisect_right(list(wl._offsets), idx) - 1
+    return np.float32(v * float(wl.tensor_scales()[t]))
+
+
+def test_numpy_path_matches_the_definition():
+    """values_np (vectorised uint64 NumPy) against Python big integers, on
+    every workload kind: tensor scales, i.i.d. scale, outliers, the pad."""
     rng = np.random.default_rng(0)
-    for name in ("tiny-n4-c4", "gpt2-small", "pythia-1.4b", "heavytail-n16-c128"):
+    for name in ("tiny-n4-c4", "iid-n8-c16-16m", "gpt2-small", "pythia-1.4b", "heavytail-n16-c128"):
         wl = synth.workload(name)
-        idx = np.unique(np.concatenate([rng.integers(0, wl.d, 20000), [0, wl.d - 1, wl.d, wl.d + 5]]))
+        idx = np.unique(np.concatenate([rng.integers(0, wl.d, 400), [0, wl.d - 1, wl.d, wl.d + 5]]))
+        if wl.tensor_sizes is not None:           # both sides of every tensor boundary
+            b = wl._offsets[1:-1]
+            idx = np.unique(np.concatenate([idx, b, b - 1]))
         for w in (0, wl.N - 1):
             a = wl.values_np(w, idx)
-            b = wl.values_torch(w, torch.from_numpy(idx)).numpy()
-            assert a.dtype == np.float32 and b.dtype == np.float32
-            np.testing.assert_array_equal(a.view(np.uint32), b.view(np.uint32))
-    key = synth.stream_key(9, 3)
-    idx = np.arange(5000)
-    np.testing.assert_array_equal(synth.normal_np(key, idx),
-                                  synth.normal_torch(key, torch.from_numpy(idx)).numpy())
-    np.testing.assert_array_equal(synth.uniform32_np(key, idx, 6),
-                                  synth.uniform32_torch(key, torch.from_numpy(idx), 6).numpy())
-
-
-def test_fill_matches_pointwise_values():
-    torch = pytest.importorskip("torch")
-    wl = synth.workload("gpt2-small")
-    out = torch.empty(10007, dtype=torch.float32)
-    wl.fill_torch(out, 2, start=wl.d - 5000, chunk=4096)
-    ref = wl.values_np(2, np.arange(wl.d - 5000, wl.d - 5000 + 10007))
-    np.testing.assert_array_equal(out.numpy(), ref)
-    assert np.all(ref[5000:] == 0)                     # beyond d: the zero pad
+            ref = np.array([_value_python(wl, w, int(i)) for i in idx], dtype=np.float32)
+            assert a.dtype == np.float32
+            np.testing.assert_array_equal(a.view(np.uint32), ref.view(np.uint32))
+    wl = synth.workload("heavytail-n16-c128")
+    assert np.abs(wl.values_np(1, np.arange(20000))).max() > 6      # outliers are in the check
 
 
 def test_irwin_hall_normal_moments():
