@@ -154,7 +154,9 @@ void cerar_plan_destroy(cerar_plan *plan);
 /* Uploads the plan's fp32 coefficient fragments and slot tables to the
  * current device, once per plan and device (hipMalloc and a synchronous
  * hipMemcpy); later calls for that device return at once.  Every enqueueing
- * call does this itself on its first use on a device.  Calling it first
+ * call does this itself on its first use on a device, except
+ * cerar_ring_simulate_noalloc, which needs it done.  It also looks up the
+ * current device's address of the no-alloc message pool.  Calling it first
  * lets a caller record the enqueueing calls into a HIP graph by stream
  * capture without an eager call, since after it they issue kernel launches
  * only.  Thread-safe.  Errors: E_INVAL (NULL plan); E_DEVICE (a HIP call
@@ -231,6 +233,30 @@ int cerar_ring_simulate(const cerar_plan *plan, size_t d,
                         const float *grads, size_t ld_grads,
                         float *work, size_t ld_work, void *ws,
                         float *out, size_t ld_out, cerar_stream stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * cerar_ring_simulate with no workspace argument.  The N*N message slots live
+ * in a static device array of the library, CERAR_NOALLOC_SCRATCH_BYTES per
+ * device, held by every device the library's code is loaded on until the
+ * process ends.  The call allocates nothing, host or device: the plan must
+ * already be on the current device (cerar_plan_prepare_device, which also
+ * sets up the array's address there), and it keeps no step record.
+ * Arguments, layouts and results are those of cerar_ring_simulate (work may
+ * equal grads for the in-place encode).  Nothing in the array needs to start
+ * at zero: every slot is written before it is read within one call.  All
+ * calls on one device share its array, so two such calls whose work can
+ * overlap in time on that device (different streams, or graph replays
+ * running concurrently) race; order them.
+ * Errors: E_INVAL (as cerar_ring_simulate, or N*N*pool_stride*4 bytes above
+ * CERAR_NOALLOC_SCRATCH_BYTES, pool_stride from cerar_chunk_len: at N = 8
+ * that is p <= 262144, d <= c * 262144); E_STATE (the plan is not on the
+ * current device); E_DEVICE. */
+#define CERAR_NOALLOC_SCRATCH_BYTES (64u << 20)
+int cerar_ring_simulate_noalloc(const cerar_plan *plan, size_t d,
+                                const float *grads, size_t ld_grads,
+                                float *work, size_t ld_work,
+                                float *out, size_t ld_out, cerar_stream stream);
 
 /* Single-GPU fused variant (not a ring implementation): the same result as
  * cerar_ring_simulate up to rounding order, computed by one kernel that runs

@@ -73,6 +73,7 @@ SIGNATURES = {
     "cerar_decode": (_I, [_P, _SZ, _P, _SZ, _P, _P, _SZ, _P]),
     "cerar_ring_simulate": (_I, [_P, _SZ, _P, _SZ, _P, _SZ, _P, _P, _SZ, _P]),
     "cerar_ring_simulate_fused": (_I, [_P, _SZ, _P, _SZ, _P, _SZ, _P]),
+    "cerar_ring_simulate_noalloc": (_I, [_P, _SZ, _P, _SZ, _P, _SZ, _P, _SZ, _P]),
     "cerar_bucketed_workspace_bytes": (_I, [_P, ctypes.POINTER(_SZ), _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ)]),
     "cerar_ring_simulate_bucketed": (_I, [_P, _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ), _P, _SZ, _P, _SZ,
                                           _P, _P, _SZ, _P]),
@@ -334,6 +335,18 @@ def ring_simulate(plan, d, grads, work, ws, out, stream=None):
     _step_buffers(plan, d, grads, work, ws, out)
     _check(lib().cerar_ring_simulate(plan.handle, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
                                      _ptr(ws), _ptr(out), _ld(out), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20          # CERAR_NOALLOC_SCRATCH_BYTES
+
+
+def ring_simulate_noalloc(plan, d, grads, work, out, stream=None):
+    """cerar_ring_simulate_noalloc: the whole all-reduce with the message pool
+    in the library's static device array (no workspace, no allocation); the
+    plan must have been prepared on the device (Plan.prepare_device)."""
+    _step_buffers(plan, d, grads, work, None, out)
+    _check(lib().cerar_ring_simulate_noalloc(plan.handle, d, _ptr(grads), _ld(grads), _ptr(work), _ld(work),
+                                             _ptr(out), _ld(out), _stream(stream)))
 
 
 def ring_simulate_fused(plan, d, grads, out, stream=None):

@@ -1905,12 +1905,63 @@ void release_device(cerar_plan *plan) {
 
 using namespace cerar;
 
+namespace cerar {
+namespace {
+
+// ---- message pool of the entry point that allocates nothing -----------------
+// cerar_ring_simulate_noalloc keeps its N*N message slots in this file-scope
+// device array instead of a caller workspace.  Each device holds its own copy
+// from the load of the library's code until the process ends.  In host code
+// the array's name is not a device address: host code uses only the address
+// hipGetSymbolAddress returns for the current device (scratch_address).
+static __device__ __align__(256) float scratch[CERAR_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch[kMaxDevices];      // per device ordinal: this device's copy of `scratch`, once looked up
+
+// Device address of the current device's `scratch`, looked up once per device
+// with that device current (the first set-up or no-alloc call on it).
+int scratch_address(float **out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(CERAR_E_DEVICE, "device ordinal %d beyond %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *ptr = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress (no-alloc message pool)");
+        g_scratch[dev] = static_cast<float *>(ptr);
+    }
+    *out = g_scratch[dev];
+    return CERAR_OK;
+}
+
+// The plan's device copy on the current device, without creating it (the
+// upload allocates): E_STATE if cerar_plan_prepare_device has not run there.
+int prepared_copy(const cerar_plan *plan, const DeviceCopy **out) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+    std::lock_guard<std::mutex> g(plan->dev_mu);
+    auto it = plan->dev.find(dev);
+    if (it == plan->dev.end())
+        return fail(CERAR_E_STATE, "the plan is not on device %d: call cerar_plan_prepare_device there first "
+                    "(its upload allocates)", dev);
+    *out = &it->second;
+    return CERAR_OK;
+}
+
+}  // namespace
+}  // namespace cerar
+
 extern "C" int cerar_plan_prepare_device(const cerar_plan *plan) {
     clear_error();
     if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
     return guarded([&] {
         const DeviceCopy *dc;
-        return device_copy(plan, &dc);
+        int st = device_copy(plan, &dc);
+        float *pool;
+        if (!st) st = scratch_address(&pool);          // set-up of the no-alloc entry point on this device
+        return st;
     });
 }
 
@@ -2006,6 +2057,49 @@ extern "C" int cerar_ring_simulate(const cerar_plan *plan, size_t d, const float
     clear_error();
     return guarded([&] {
         return ring_simulate_impl(plan, d, grads, ld_grads, work, ld_work, ws, out, ld_out, stream);
+    });
+}
+
+// No device or host allocation on this path: the geometry and the size check
+// are host arithmetic, the plan's device copy must already exist, the pool is
+// the static array, and the rest is kernel launches (no step record either).
+static int ring_simulate_noalloc_impl(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                      float *work, size_t ld_work, float *out, size_t ld_out,
+                                      cerar_stream stream) {
+    if (!plan) return fail(CERAR_E_INVAL, "plan is NULL");
+    size_t p, stride;
+    int st = cerar_chunk_len(plan, d, &p, &stride);
+    if (st) return st;
+    const size_t need = (size_t)plan->tab.pool_slots() * stride * sizeof(float);
+    if (need > (size_t)CERAR_NOALLOC_SCRATCH_BYTES)
+        return fail(CERAR_E_INVAL, "N=%d, d=%zu needs %zu bytes of message pool (N*N slots of %zu floats); "
+                    "the no-alloc pool holds %zu", plan->N, d, need, stride, (size_t)CERAR_NOALLOC_SCRATCH_BYTES);
+    const DeviceCopy *dc;
+    st = prepared_copy(plan, &dc);
+    if (st) return st;
+    float *ws;
+    st = scratch_address(&ws);
+    if (st) return st;
+    Geometry g;
+    st = check_common(plan, d, work, ld_work, ws, g);
+    if (st) return st;
+    st = check_grads(plan, d, grads, ld_grads, work, ld_work, ws, g);
+    if (st) return st;
+    st = check_out(plan, d, work, ld_work, ws, out, ld_out, g);
+    if (st) return st;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    st = enqueue_encode(plan, dc, g, d, grads, ld_grads, work, ld_work, ws, s);
+    for (int k = 1; k <= plan->L && !st; ++k) st = enqueue_round(plan, dc, g, k, work, ld_work, ws, s);
+    if (!st) st = enqueue_decode(plan, dc, g, d, work, ld_work, ws, out, ld_out, s);
+    return st;
+}
+
+extern "C" int cerar_ring_simulate_noalloc(const cerar_plan *plan, size_t d, const float *grads, size_t ld_grads,
+                                           float *work, size_t ld_work, float *out, size_t ld_out,
+                                           cerar_stream stream) {
+    clear_error();
+    return guarded([&] {
+        return ring_simulate_noalloc_impl(plan, d, grads, ld_grads, work, ld_work, out, ld_out, stream);
     });
 }
 

@@ -1,0 +1,87 @@
+"""cerar_ring_simulate_noalloc, the entry point for callers that cannot
+allocate: its message pool is the library's static device array, not a
+caller workspace.  Through the C ABI it must give the bits of
+cerar_ring_simulate on the same inputs, on consecutive calls of different
+sizes (the array keeps the previous call's contents), refuse a pool larger
+than the array, and refuse a plan that is not yet on the device."""
+
+import numpy as np
+import pytest
+
+from paper_2609_23898_amd import cerar as C
+
+from gpu_util import buffers, host_grads, max_rel_l2, oracle_allreduce, orthogonal_plan, to_device, torch_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_both(plan, U, R, d, seed, in_place=False):
+    torch, dev = torch_dev()
+    g = host_grads(plan.N, d, seed=seed)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    p, _ = plan.chunk_len(d)
+    if in_place:
+        a = to_device(np.pad(g, ((0, 0), (0, plan.c * p - d))), ld=plan.c * p)
+        out2 = torch.full_like(out, float("nan"))
+        C.ring_simulate_noalloc(plan, d, a, a, out2)
+    else:
+        work2, _, out2 = buffers(plan, d)
+        C.ring_simulate_noalloc(plan, d, grads, work2, out2)
+    torch.cuda.synchronize()
+    assert bool(torch.equal(out, out2)), "no-alloc result differs from cerar_ring_simulate"
+    assert max_rel_l2(out2.double().cpu().numpy(), oracle_allreduce(g, U, R)) <= 1e-4
+
+
+def test_noalloc_matches_ring_simulate_on_consecutive_calls():
+    """Two calls in a row, the second smaller (the pool keeps the first
+    call's values in the slots the second does not use), then a different
+    plan and an in-place encode on the same array."""
+    N, c = 8, 64
+    U, R = orthogonal_plan(N, c, seed=71)
+    plan = C.Plan.explicit(U, R)
+    plan.prepare_device()
+    _run_both(plan, U, R, 64 * 4000 + 13, seed=71)        # p = 4032: 8 MiB of the pool
+    _run_both(plan, U, R, 64 * 900 + 5, seed=72)          # smaller
+    U2, R2 = orthogonal_plan(4, 16, seed=73)
+    plan2 = C.Plan.explicit(U2, R2)
+    plan2.prepare_device()
+    _run_both(plan2, U2, R2, 16 * 3000 + 7, seed=73, in_place=True)
+
+
+def test_noalloc_limits_and_preconditions():
+    torch, dev = torch_dev()
+    N, c = 8, 64
+    U, R = orthogonal_plan(N, c, seed=74)
+    fresh = C.Plan.explicit(U, R)                          # not prepared on the device
+    d = 64 * 100
+    grads = to_device(host_grads(N, d, seed=74))
+    work, _, out = buffers(fresh, d)
+    with pytest.raises(C.CerarError) as ei:
+        C.ring_simulate_noalloc(fresh, d, grads, work, out)
+    assert ei.value.status == -6 and "prepare_device" in str(ei.value)
+    fresh.prepare_device()
+    # the largest d whose pool fits the array, and the next chunk length up
+    p_max = C.NOALLOC_SCRATCH_BYTES // (4 * N * N)
+    assert p_max % 64 == 0
+    big_ok, big_bad = c * p_max, c * p_max + 1
+    assert fresh.workspace_bytes(big_ok) == C.NOALLOC_SCRATCH_BYTES
+    assert fresh.workspace_bytes(big_bad) > C.NOALLOC_SCRATCH_BYTES
+    gb = torch.zeros((N, big_bad), dtype=torch.float32, device=dev)
+    wb = torch.zeros((N, c * fresh.chunk_len(big_bad)[0]), dtype=torch.float32, device=dev)
+    ob = torch.zeros((N, big_bad), dtype=torch.float32, device=dev)
+    with pytest.raises(C.CerarError) as ei:
+        C.ring_simulate_noalloc(fresh, big_bad, gb, wb, ob)
+    assert ei.value.status == -1 and "no-alloc pool" in str(ei.value)
+    # the largest size runs and matches the workspace call
+    del gb, wb, ob
+    g = torch.zeros((N, big_ok), dtype=torch.float32, device=dev)
+    for w in range(N):
+        g[w].normal_(generator=torch.Generator(device=dev).manual_seed(w))
+    work, ws, out = buffers(fresh, big_ok)
+    C.ring_simulate(fresh, big_ok, g, work, ws, out)
+    work2, _, out2 = buffers(fresh, big_ok)
+    C.ring_simulate_noalloc(fresh, big_ok, g, work2, out2)
+    torch.cuda.synchronize()
+    assert bool(torch.equal(out, out2))
