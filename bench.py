@@ -182,7 +182,10 @@ def summarize_trace(trace_dir, bench_log, out_path, bench_args=()):
     print("\n".join(lines))
 
 
-def _pmc_per_family(d, counter):
+def _pmc_per_family(d, counter, copy_grid=None):
+    """Mean counter value per dispatch of each family.  The copy kernel also
+    serves the bench's refills of other sizes: with copy_grid, only its
+    dispatches of that grid size (the reference copy) count."""
     rows = _read_csv(_find_csv(d, "counter_collection.csv"))
     acc = {}
     for r in rows:
@@ -191,14 +194,16 @@ def _pmc_per_family(d, counter):
         fam = family_of_name(r["Kernel_Name"])
         if fam is None:
             continue
+        if fam.startswith("k_copy4") and copy_grid is not None and int(r["Grid_Size"]) != copy_grid:
+            continue
         v, n = acc.get(fam, (0.0, 0))
         acc[fam] = (v + float(r["Counter_Value"]), n + 1)
     return {fam: (v / n, n) for fam, (v, n) in acc.items()}
 
 
 def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30):
-    fetch = _pmc_per_family(fetch_dir, "FETCH_SIZE")
-    write = _pmc_per_family(write_dir, "WRITE_SIZE")
+    fetch = _pmc_per_family(fetch_dir, "FETCH_SIZE", copy_grid=copy_floats // 4)
+    write = _pmc_per_family(write_dir, "WRITE_SIZE", copy_grid=copy_floats // 4)
     copy = "k_copy4 (copy reference)"
     copy_kib = copy_floats * 4 / 1024.0
     f_scale = fetch[copy][0] / copy_kib

@@ -73,13 +73,15 @@ def test_counter_summary_is_scaled_by_the_copy_kernel(tmp_path):
     copy_floats = 1 << 20
     copy_kib = copy_floats * 4 / 1024
     enc = "void cerar::(anonymous namespace)::k_encode_dbuf<16, 4>(cerar::(anonymous namespace)::EncParams)"
-    hdr = ["Kernel_Name", "Counter_Name", "Counter_Value"]
+    hdr = ["Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"]
+    g = copy_floats // 4
+    # the bench's other copies (gradient refills, 3x as long) must not enter the scale
     _write_csv(str(tmp_path / "fetch" / "host" / "pmc_counter_collection.csv"), hdr,
-               [["k_copy4", "FETCH_SIZE", copy_kib * 0.5], [f'"{enc}"', "FETCH_SIZE", 1000.0],
-                [f'"{enc}"', "FETCH_SIZE", 1200.0]])
+               [["k_copy4", g, "FETCH_SIZE", copy_kib * 0.5], ["k_copy4", 3 * g, "FETCH_SIZE", copy_kib * 1.5],
+                [f'"{enc}"', 4096, "FETCH_SIZE", 1000.0], [f'"{enc}"', 4096, "FETCH_SIZE", 1200.0]])
     _write_csv(str(tmp_path / "write" / "host" / "pmc_counter_collection.csv"), hdr,
-               [["k_copy4", "WRITE_SIZE", copy_kib], [f'"{enc}"', "WRITE_SIZE", 3000.0],
-                [f'"{enc}"', "WRITE_SIZE", 3000.0]])
+               [["k_copy4", g, "WRITE_SIZE", copy_kib], ["k_copy4", 3 * g, "WRITE_SIZE", 3 * copy_kib],
+                [f'"{enc}"', 4096, "WRITE_SIZE", 3000.0], [f'"{enc}"', 4096, "WRITE_SIZE", 3000.0]])
     out = tmp_path / "summary.txt"
     bench.summarize_pmc(str(tmp_path / "fetch"), str(tmp_path / "write"), str(out), copy_floats=copy_floats)
     text = out.read_text()
