@@ -244,10 +244,11 @@ __device__ inline void mtile2_mma_lds2(v4f (&acc)[2][2], const v2f (&b)[KS], con
 
 // Copies nmt M-tiles of fragments [mt][ks][lane] (KSx K-steps) into LDS as
 // [mt][q][lane][r], ks = 4q + r, zero-padded to KSpad K-steps.
-__device__ inline void stage_fragments_padded(float *sfrag, const float *gfrag, int nmt, int KSx, int KSpad) {
+__device__ inline void stage_fragments_padded(float *sfrag, const float *gfrag, int nmt, int KSx, int KSpad,
+                                              int nthreads = kThreads) {
     const int Q = (KSpad + 3) / 4;
     const int total = nmt * Q * 256;
-    for (int idx = threadIdx.x; idx < total; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < total; idx += nthreads) {
         const int r = idx & 3, ln = (idx >> 2) & 63, q = (idx >> 8) % Q, mt = (idx >> 8) / Q;
         const int ks = q * 4 + r;
         sfrag[idx] = ks < KSx ? gfrag[((size_t)mt * KSx + ks) * 64 + ln] : 0.f;
@@ -549,77 +550,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     unsigned bid;
     const EncParams a = b.at(bid);
     k_encode_dbuf_body<KS, MTC>(a, bid);
-}
-
-// Wide encode for c = 16 MTC > 64: at 2c flops per byte the contraction is
-// bound by the fp32 MFMA rate, so one wave per SIMD runs it with two register
-// buffers of B operands: half-block n+1's loads are in flight while half-block
-// n's MTC M-tiles run, and each tile's 16 output rows are stored as soon as it
-// is done.  Half-blocks of 32 positions (a float2 per lane and K-step) keep
-// both buffers in the architectural registers.
-template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_encode_wide(EncParams a) {
-    static_assert(MTC % 2 == 0, "M-tiles run in pairs");
-    extern __shared__ float sfrag[];
-    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
-    const int wg = blockIdx.x / a.N;
-    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int col = lane & 15, krow = lane >> 4;
-    const int KSx = a.KSe;
-    constexpr int Q = (KS + 3) / 4;
-    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS);
-    __syncthreads();
-    const float *src = a.grads + (size_t)worker * a.ld_g;
-    float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
-    float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
-    const size_t p = a.sb.p;
-    // half-blocks of 32 positions: [2 blk0, 2 blk1)
-    const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
-                 end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
-    size_t hb = first + wave;
-    if (hb >= end) return;
-    v2f b0[KS], b1[KS];
-    auto load = [&](v2f (&b)[KS], size_t h) {
-        const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 2 * (size_t)col) * sizeof(float)));
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) b[ks] = load2_off(src + h * 32 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
-    };
-    auto tile = [&](const v2f (&b)[KS], size_t h, int mt) {     // M-tiles mt and mt + 1
-        const size_t e0 = h * 32;
-        const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
-        v4f acc[2][2];
-        mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const v2f v = {acc[m][0][r], acc[m][1][r]};
-                nt_store2_off(dst + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
-                if (mt + m == 0 && krow * 4 + r == 0) nt_store2_off(x1 + e0, (uint32_t)(2 * col * sizeof(float)), v);
-            }
-    };
-    // the next half-block's loads go out after the first M-tile pair, when this
-    // half-block's operands have all arrived.  The loop header precedes the
-    // first pair, so every other half-block waits for the previous stores to
-    // drain; a header after the first pair measured slower here, since the
-    // third copy of the pair's code costs scalar-register spills.
-    load(b0, hb);
-    while (true) {
-        size_t next = hb + kWaves;
-        tile(b0, hb, 0);
-        if (next < end) load(b1, next);
-#pragma unroll
-        for (int mt = 2; mt < MTC; mt += 2) tile(b0, hb, mt);
-        if (next >= end) break;
-        hb = next;
-        next = hb + kWaves;
-        tile(b1, hb, 0);
-        if (next < end) load(b0, next);
-#pragma unroll
-        for (int mt = 2; mt < MTC; mt += 2) tile(b1, hb, mt);
-        if (next >= end) break;
-        hb = next;
-    }
 }
 
 // ---- K2/K3: one ring round ---------------------------------------------------
@@ -990,8 +920,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     k_decode_dbuf_body<KS, MTC>(a, bid);
 }
 
-// Wide decode for c = 16 MTC > 64, same scheme as the wide encode; the B
-// rows come through the per-worker table of observation slots.
+// Wide decode for c = 16 MTC > 64 with more observations than the
+// four-wave kernel below holds in LDS twice per CU (K > 144): at 2(L+1)c
+// flops per position the contraction is bound by the fp32 MFMA rate, so one
+// wave per SIMD runs it with two register buffers of B operands: half-block
+// n+1's loads are in flight while half-block n's MTC M-tiles run, and each
+// tile's 16 output rows are stored as soon as it is done.  Half-blocks of 32
+// positions (a float2 per lane and K-step) keep both buffers in the
+// architectural registers.  The B rows come through the per-worker table of
+// observation slots.
 template <int KS, int MTC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_decode_wide(DecParams a) {
     static_assert(MTC % 2 == 0, "M-tiles run in pairs");
@@ -1053,6 +990,100 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
         for (int mt = 2; mt < MTC; mt += 2) tile(b1, hb, mt);
         if (next >= end) break;
         hb = next;
+    }
+}
+
+// c = 128 with four waves per SIMD (measured 11 % faster for the encode and
+// 6 % for the decode than one double-buffered wave per SIMD, which leaves
+// nothing to cover a wave's own waits).  512-thread workgroups
+// (8 waves) share one LDS copy of the coefficient fragments (64 KiB for the
+// encode, 72 KiB for the decode at K <= 144), two workgroups fit a CU, and
+// each wave keeps a single buffer of B operands within 128 registers: while
+// one wave waits for its half-block's loads, the other waves on its SIMD
+// keep the MFMA pipe busy.
+constexpr int kWideWaves = 8;
+
+template <int KS, int MTC>
+__global__ __launch_bounds__(64 * kWideWaves) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_encode_wide_sb(EncParams a) {
+    static_assert(MTC % 2 == 0, "M-tiles run in pairs");
+    extern __shared__ float sfrag[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int KSx = a.KSe;
+    constexpr int Q = (KS + 3) / 4;
+    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS, 64 * kWideWaves);
+    __syncthreads();
+    const float *src = a.grads + (size_t)worker * a.ld_g;
+    float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
+    float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
+    const size_t p = a.sb.p;
+    // half-blocks of 32 positions: [2 blk0, 2 blk1)
+    const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
+                 end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
+    for (size_t hb = first + wave; hb < end; hb += kWideWaves) {
+        v2f b[KS];
+        const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 2 * (size_t)col) * sizeof(float)));
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = load2_off(src + hb * 32 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+        const size_t e0 = hb * 32;
+#pragma unroll
+        for (int mt = 0; mt < MTC; mt += 2) {        // M-tiles mt and mt + 1
+            const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
+            v4f acc[2][2];
+            mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const v2f v = {acc[m][0][r], acc[m][1][r]};
+                    nt_store2_off(dst + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
+                    if (mt + m == 0 && krow * 4 + r == 0) nt_store2_off(x1 + e0, (uint32_t)(2 * col * sizeof(float)), v);
+                }
+        }
+    }
+}
+
+template <int KS, int MTC>
+__global__ __launch_bounds__(64 * kWideWaves) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_decode_wide_sb(DecParams a) {
+    static_assert(MTC % 2 == 0, "M-tiles run in pairs");
+    extern __shared__ float smem[];
+    const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
+    const int wg = blockIdx.x / a.N;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int col = lane & 15, krow = lane >> 4;
+    const int KSx = a.KSd;
+    constexpr int Q = (KS + 3) / 4;
+    float *sfrag = smem;
+    const float **srow = reinterpret_cast<const float **>(smem + (size_t)MTC * Q * 256);
+    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS, 64 * kWideWaves);
+    // rows K..4 KS-1 repeat row K-1, whose coefficients there are zero
+    for (int t = threadIdx.x; t < 4 * KS; t += 64 * kWideWaves)
+        srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
+    __syncthreads();
+    float *out = a.out + (size_t)worker * a.ld_o;
+    const size_t p = a.sb.p;
+    const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
+                 end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
+    for (size_t hb = first + wave; hb < end; hb += kWideWaves) {
+        v2f b[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load2_g(srow[ks * 4 + krow] + hb * 32 + 2 * col);
+        const size_t e0 = hb * 32;
+#pragma unroll
+        for (int mt = 0; mt < MTC; mt += 2) {        // M-tiles mt and mt + 1
+            const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
+            v4f acc[2][2];
+            mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const v2f v = {acc[m][0][r], acc[m][1][r]};
+                    nt_store2_off(out + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
+                }
+        }
     }
 }
 
@@ -1746,8 +1777,8 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
             w.blk0 = 0;
             w.blk1 = bs.interior;
             wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
-            hipLaunchKernelGGL((k_encode_wide<32, 8>), dim3((unsigned)(N * w.wg_per_worker)), dim3(kThreads),
-                               (size_t)8 * 8 * 256 * sizeof(float), s, w);
+            hipLaunchKernelGGL((k_encode_wide_sb<32, 8>), dim3((unsigned)(N * w.wg_per_worker)),
+                               dim3(64 * kWideWaves), (size_t)8 * 8 * 256 * sizeof(float), s, w);
             if (bs.total > bs.interior) {
                 EncParams t = a;
                 t.blk0 = bs.interior;
@@ -1833,7 +1864,7 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
         wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
         const dim3 grid((unsigned)(N * w.wg_per_worker));
         auto lds_for = [](int K4) { return (size_t)8 * (K4 / 4) * 256 * sizeof(float) + (size_t)4 * K4 * sizeof(float *); };
-        if (ks <= 36) hipLaunchKernelGGL((k_decode_wide<36, 8>), grid, dim3(kThreads), lds_for(36), s, w);
+        if (ks <= 36) hipLaunchKernelGGL((k_decode_wide_sb<36, 8>), grid, dim3(64 * kWideWaves), lds_for(36), s, w);
         else if (ks <= 40) hipLaunchKernelGGL((k_decode_wide<40, 8>), grid, dim3(kThreads), lds_for(40), s, w);
         else if (ks <= 44) hipLaunchKernelGGL((k_decode_wide<44, 8>), grid, dim3(kThreads), lds_for(44), s, w);
         else hipLaunchKernelGGL((k_decode_wide<48, 8>), grid, dim3(kThreads), lds_for(48), s, w);
