@@ -34,6 +34,7 @@ METRIC = "encode+round+decode GB/s per worker (% HBM peak), N=8 c=64 d=1.4e9 fp3
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 CPU_WORKERS_MAX = 15
+ORACLE_KEEP = 1024                 # oracle outputs kept per process for the GPU line's parity
 
 
 def log(msg):
@@ -271,7 +272,7 @@ def family_of(k, N, c, L):
     return None
 
 
-def _oracle_worker(name, pos, U, R, seconds, barrier, queue):
+def _oracle_worker(name, pos, U, R, seconds, keep, barrier, queue):
     """One host process of the CPU baseline: draws the oracle's inputs at its
     positions from the shared generator, waits for the other processes, then
     runs the fp64 oracle (encode, Algorithm 1 in lock-step, decode) on one
@@ -298,13 +299,16 @@ def _oracle_worker(name, pos, U, R, seconds, barrier, queue):
                 if t1 - t0 >= seconds:
                     break
         finite = all(bool(np.all(np.isfinite(o))) for o in out)
-        queue.put((t0, t1, reps * len(pos), finite, None))
+        # the oracle's outputs at the first `keep` positions, for the GPU line's parity
+        keep_pos = pos[:keep]
+        keep_out = np.stack([o[:keep] for o in out])            # N x keep x c
+        queue.put((t0, t1, reps * len(pos), finite, None, keep_pos, keep_out))
     except Exception as e:                          # reported by the parent
         try:
             barrier.abort()
         except Exception:
             pass
-        queue.put((0.0, 0.0, 0, False, repr(e)))
+        queue.put((0.0, 0.0, 0, False, repr(e), None, None))
 
 
 def cpu_baseline(name, U, R, plan_desc, positions, seconds):
@@ -336,7 +340,7 @@ def cpu_baseline(name, U, R, plan_desc, positions, seconds):
     parts = np.array_split(pos_all, threads)
     ctx = mp.get_context("fork")
     barrier, queue = ctx.Barrier(threads), ctx.Queue()
-    procs = [ctx.Process(target=_oracle_worker, args=(name, part, U, R, seconds, barrier, queue))
+    procs = [ctx.Process(target=_oracle_worker, args=(name, part, U, R, seconds, ORACLE_KEEP, barrier, queue))
              for part in parts]
     for pr in procs:
         pr.start()
@@ -353,7 +357,8 @@ def cpu_baseline(name, U, R, plan_desc, positions, seconds):
     rates = sorted(r[2] * per_pos / (r[1] - r[0]) / 1e9 for r in res)
     step_bytes = N * (8 * c + 3 * N - 9) * p * 4
     value = done * per_pos / wall / 1e9
-    return {"value": round(value, 4), "unit": "GB/s", "cores": cores, "threads": threads, "kind": "oracle",
+    reference = (np.concatenate([r[5] for r in res]), np.concatenate([r[6] for r in res], axis=1))
+    return reference, {"value": round(value, 4), "unit": "GB/s", "cores": cores, "threads": threads, "kind": "oracle",
             "seconds": round(wall, 2), "per_thread_gbps_median": round(rates[len(rates) // 2], 4),
             "extrapolated_step_s": round(step_bytes / (value * 1e9), 1),
             "plan": "the GPU line's plan (its fp64 U and R, from cerar_plan_get_matrices)",
@@ -459,7 +464,8 @@ def main():
     if args.cpu_positions > 0:
         t = time.perf_counter()
         U_plan, R_plan = plan.matrices()
-        cpu = cpu_baseline(args.workload, U_plan, R_plan, plan_desc, args.cpu_positions, args.cpu_seconds)
+        oracle_ref, cpu = cpu_baseline(args.workload, U_plan, R_plan, plan_desc, args.cpu_positions,
+                                       args.cpu_seconds)
         log(f"cpu baseline: {cpu['value']:.3f} GB/s on {cpu['threads']} processes "
             f"({time.perf_counter() - t:.1f}s total)")
 
@@ -631,6 +637,23 @@ def main():
     C.error_norms(N, d, grads, out, norms)
     nm = norms.cpu().numpy()
     rel_err = [math.sqrt(nm[i] / nm[N]) for i in range(N)]
+    # parity of this run's outputs with the oracle at the CPU baseline's
+    # positions (K5's parity term, cerar_sampled_norms)
+    parity = None
+    if cpu is not None:
+        pos, ref = oracle_ref                                  # ref: N x S x c, chunk m at position e
+        flat = (np.arange(c)[None, :] * p + pos[:, None])      # S x c flat output indices
+        ok = flat < d
+        idx = torch.from_numpy(np.ascontiguousarray(flat[ok], dtype=np.int64)).to(dev)
+        refv = torch.from_numpy(np.ascontiguousarray(ref[:, ok])).to(dev)
+        pn = torch.empty(2 * N, dtype=torch.float64, device=dev)
+        C.sampled_norms(N, d, idx, refv, out, pn)
+        pv = pn.cpu().numpy()
+        parity = {"max_rel_l2": max(math.sqrt(pv[2 * i] / pv[2 * i + 1]) for i in range(N)),
+                  "outputs": int(ok.sum()) * N, "kappa_M": info["kappa_M"],
+                  "note": "the GPU line's outputs against the fp64 oracle of cpu_baseline on the same plan and "
+                          "inputs, at its kept positions; squared sums by K5 (cerar_sampled_norms)"}
+        log(f"parity vs oracle: {parity['max_rel_l2']:.3g} over {parity['outputs']} outputs")
 
     step_bytes = N * C.algorithmic_bytes_per_worker(N, c, p)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
@@ -660,6 +683,7 @@ def main():
         "encode_spread": spread,
         "copy_gbps": round(copy_gbps, 1),
         "approx_rel_err_max": max(rel_err),
+        "parity_vs_oracle": parity,
         "plan_info": {k: info[k] for k in ("kappa_M", "kappa_U", "kappa_R", "phi", "phi_closed_form",
                                             "comm_rate", "storage_rate", "r_star", "fp64_reliable")},
     }

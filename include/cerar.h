@@ -100,6 +100,10 @@ typedef struct {
     int n_node_perms;       /* 0: H as above (perturb, else diag(nodes)); at most 4096 */
     int svd_sweeps;         /* cap on the sweeps of each one-sided Jacobi SVD (the projection,
                              * kappa, gamma and ||H||); 0 selects 80 */
+    int als_restarts;       /* KAPPA: ALS runs from the O(eps0) plans of different random bases
+                             * B (seeds seed, seed + 8, seed + 16, ...; the problem of
+                             * Sec. II-D is nonconvex); the plan with the least Phi is kept.
+                             * 0 or 1: one run.  At most 64; needs base == NULL */
 } cerar_plan_desc;
 
 /* Plan diagnostics (host fp64). */
@@ -126,6 +130,8 @@ typedef struct {
                                    * kappa_R, amplification, gamma and ||H||_2 converged within the
                                    * sweep cap; 0 when one stopped at the cap (those figures are
                                    * then approximate) */
+    int restart_used;             /* KAPPA: index of the ALS restart kept (0 = the first run);
+                                   * -1 for other constructions */
 } cerar_plan_info;
 
 /* Build a plan on the host in fp64 (Sec. II-B to II-D): B and D (or the
@@ -306,6 +312,19 @@ int cerar_ring_simulate_bucketed(const cerar_plan *plan, int nbuckets,
 int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_grads,
                       const float *out, size_t ld_out, double *norms,
                       cerar_stream stream);
+
+/* K5's parity term on sampled positions: the relative l2 difference between
+ * the device's outputs and an independent computation of them (the fp64
+ * CPU implementation of the tests and the bench) at the positions it
+ * computed.  For every worker i < N: norms[2i] = sum_t (out[i*ld_out +
+ * idx[t]] - ref[i*count + t])^2 and norms[2i+1] = sum_t ref[i*count + t]^2,
+ * in fp64.  idx: device int64[count] flat output indices, each in [0, d)
+ * (one outside makes that worker's sums NaN); ref: device fp64, N x count;
+ * out: device fp32, N rows of stride ld_out; norms: device, 2N doubles,
+ * overwritten.  Errors: E_INVAL (N outside [1, 64], count == 0, d == 0,
+ * NULL buffers, ld_out < d); E_DEVICE. */
+int cerar_sampled_norms(int N, size_t count, size_t d, const int64_t *idx, const double *ref,
+                        const float *out, size_t ld_out, double *norms, cerar_stream stream);
 
 /* Measurement helper: dst[0..n) = src[0..n), a plain streaming copy used as
  * the achievable-bandwidth reference and as the known-size kernel that

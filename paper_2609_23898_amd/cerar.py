@@ -36,7 +36,7 @@ class PlanDesc(ctypes.Structure):
                 ("nodes", ctypes.POINTER(ctypes.c_double)),
                 ("eps0", ctypes.c_double), ("als_iters", ctypes.c_int), ("als_order", ctypes.c_int),
                 ("node_perms", ctypes.POINTER(ctypes.c_int)), ("n_node_perms", ctypes.c_int),
-                ("svd_sweeps", ctypes.c_int)]
+                ("svd_sweeps", ctypes.c_int), ("als_restarts", ctypes.c_int)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -49,7 +49,7 @@ class PlanInfo(ctypes.Structure):
                 ("storage_rate", ctypes.c_double), ("proj_a0", ctypes.c_double),
                 ("proj_b0", ctypes.c_double), ("fp64_reliable", ctypes.c_int),
                 ("seed_used", ctypes.c_uint64), ("gamma", ctypes.c_double), ("h_choice", ctypes.c_int),
-                ("svd_converged", ctypes.c_int)]
+                ("svd_converged", ctypes.c_int), ("restart_used", ctypes.c_int)]
 
 
 _P = ctypes.c_void_p
@@ -78,6 +78,7 @@ SIGNATURES = {
     "cerar_ring_simulate_bucketed": (_I, [_P, _I, ctypes.POINTER(_SZ), ctypes.POINTER(_SZ), _P, _SZ, _P, _SZ,
                                           _P, _P, _SZ, _P]),
     "cerar_error_norms": (_I, [_I, _SZ, _P, _SZ, _P, _SZ, _P, _P]),
+    "cerar_sampled_norms": (_I, [_I, _SZ, _SZ, _P, _P, _P, _SZ, _P, _P]),
     "cerar_copy_f32": (_I, [_P, _P, _SZ, _P]),
     "cerar_synth_fill": (_I, [_P, _SZ, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, _P, _P, _I,
                               ctypes.c_uint32, ctypes.c_double, _P]),
@@ -139,7 +140,8 @@ class Plan:
     """Encoding/decoding plan (host fp64), see cerar_plan_create_desc."""
 
     def __init__(self, N, c, kind, param=0.0, seed=0, base=None, perturb=None, nodes=None,
-                 eps0=0.0, als_iters=0, als_order=0, node_perms=None, svd_sweeps=0, _handle=None):
+                 eps0=0.0, als_iters=0, als_order=0, node_perms=None, svd_sweeps=0, als_restarts=0,
+                 _handle=None):
         L = lib()
         self._h = _P()
         if _handle is not None:
@@ -164,7 +166,7 @@ class Plan:
                 perms, nperm = pa.ctypes.data_as(ctypes.POINTER(ctypes.c_int)), pa.shape[0]
             desc = PlanDesc(N, c, kind, float(param), int(seed), arr(base, N * c),
                             arr(perturb, c * c), arr(nodes, c), float(eps0), int(als_iters),
-                            int(als_order), perms, nperm, int(svd_sweeps))
+                            int(als_order), perms, nperm, int(svd_sweeps), int(als_restarts))
             _check(L.cerar_plan_create_desc(ctypes.byref(desc), ctypes.byref(self._h)))
         info = self.info()
         self.N, self.c, self.L = info["N"], info["c"], info["L"]
@@ -379,6 +381,24 @@ def error_norms(N, d, grads, out, norms, stream=None):
         raise ValueError(f"norms must be a contiguous float64 tensor of at least {N + 1} entries")
     _check(lib().cerar_error_norms(N, d, _ptr(grads), _ld(grads), _ptr(out), _ld(out), _ptr(norms),
                                    _stream(stream)))
+
+
+def sampled_norms(N, d, idx, ref, out, norms, stream=None):
+    """K5's parity term (cerar_sampled_norms): idx an int64 device tensor of
+    flat output indices, ref an (N, len(idx)) float64 device tensor, norms a
+    float64 device tensor of 2N entries."""
+    _rows(out, "out", N, d)
+    _on_device(idx, "idx")
+    _on_device(ref, "ref")
+    _on_device(norms, "norms")
+    if str(idx.dtype) != "torch.int64" or idx.dim() != 1 or not idx.is_contiguous() or idx.numel() == 0:
+        raise ValueError("idx must be a non-empty contiguous 1-D int64 tensor")
+    if str(ref.dtype) != "torch.float64" or not ref.is_contiguous() or tuple(ref.shape) != (N, idx.numel()):
+        raise ValueError(f"ref must be a contiguous float64 tensor of shape ({N}, {idx.numel()})")
+    if str(norms.dtype) != "torch.float64" or not norms.is_contiguous() or norms.numel() < 2 * N:
+        raise ValueError(f"norms must be a contiguous float64 tensor of at least {2 * N} entries")
+    _check(lib().cerar_sampled_norms(N, idx.numel(), d, _ptr(idx), _ptr(ref), _ptr(out), _ld(out), _ptr(norms),
+                                     _stream(stream)))
 
 
 def copy_f32(dst, src, stream=None):

@@ -1433,6 +1433,39 @@ __global__ __launch_bounds__(kThreads) void k_norms(int N, size_t d, const float
     }
 }
 
+// K5's parity term: per worker w (blockIdx.y), the squared difference between
+// the device outputs at sampled flat indices and reference values computed
+// elsewhere, and the squared reference, in fp64.  An index outside [0, d)
+// contributes NaN instead of being read.
+__global__ __launch_bounds__(kThreads) void k_sampled_norms(size_t count, size_t d, const int64_t *__restrict__ idx,
+                                                           const double *__restrict__ ref, const float *__restrict__ out,
+                                                           size_t ld_o, double *norms) {
+    __shared__ double red[kWaves][2];
+    const int w = blockIdx.y;
+    double dd = 0.0, rr = 0.0;
+    for (size_t t = (size_t)blockIdx.x * kThreads + threadIdx.x; t < count; t += (size_t)gridDim.x * kThreads) {
+        const double r = ref[(size_t)w * count + t];
+        const int64_t e = idx[t];
+        const double g = (e >= 0 && (uint64_t)e < d) ? (double)out[(size_t)w * ld_o + (size_t)e] : __builtin_nan("");
+        const double diff = g - r;
+        dd += diff * diff;
+        rr += r * r;
+    }
+    dd = wave_sum(dd);
+    rr = wave_sum(rr);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) {
+        red[wave][0] = dd;
+        red[wave][1] = rr;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        double v = 0.0;
+        for (int q = 0; q < kWaves; ++q) v += red[q][threadIdx.x];
+        atomicAdd(norms + 2 * w + threadIdx.x, v);
+    }
+}
+
 // ---- copy ----------------------------------------------------------------------
 
 constexpr int kCopyThreads = 64;
@@ -2265,6 +2298,23 @@ extern "C" int cerar_error_norms(int N, size_t d, const float *grads, size_t ld_
     const dim3 grid((unsigned)blocks, (unsigned)((N + kNormWorkers - 1) / kNormWorkers));
     hipLaunchKernelGGL(k_norms, grid, dim3(kThreads), 0, s, N, d, grads, ld_grads, out, ld_out, norms);
     HIP_TRY(hipGetLastError(), "launch norms");
+    return CERAR_OK;
+}
+
+extern "C" int cerar_sampled_norms(int N, size_t count, size_t d, const int64_t *idx, const double *ref,
+                                   const float *out, size_t ld_out, double *norms, cerar_stream stream) {
+    clear_error();
+    if (N < 1 || N > kMaxN) return fail(CERAR_E_INVAL, "N=%d outside [1, %d]", N, kMaxN);
+    if (count == 0 || d == 0 || !idx || !ref || !out || !norms)
+        return fail(CERAR_E_INVAL, "count > 0, d > 0 and non-NULL buffers required");
+    if (ld_out < d) return fail(CERAR_E_INVAL, "ld_out=%zu < d=%zu", ld_out, d);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(k_fill_zero, dim3(1), dim3(128), 0, s, norms, 2 * N);
+    HIP_TRY(hipGetLastError(), "launch fill");
+    const size_t blocks = std::min<size_t>((count + kThreads - 1) / kThreads, 1024);
+    hipLaunchKernelGGL(k_sampled_norms, dim3((unsigned)blocks, (unsigned)N), dim3(kThreads), 0, s, count, d, idx, ref,
+                       out, ld_out, norms);
+    HIP_TRY(hipGetLastError(), "launch sampled norms");
     return CERAR_OK;
 }
 

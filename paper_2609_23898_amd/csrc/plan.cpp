@@ -375,6 +375,10 @@ int validate(const cerar_plan_desc *d) {
             return fail(CERAR_E_INVAL, "unknown construction %d", (int)d->kind);
     }
     if (d->svd_sweeps < 0) return fail(CERAR_E_INVAL, "svd_sweeps=%d must be >= 0", d->svd_sweeps);
+    if (d->als_restarts < 0 || d->als_restarts > 64)
+        return fail(CERAR_E_INVAL, "als_restarts=%d outside [0, 64]", d->als_restarts);
+    if (d->als_restarts > 1 && d->base)
+        return fail(CERAR_E_INVAL, "als_restarts draw new random bases B: not with a given base");
     if (d->n_node_perms < 0 || d->n_node_perms > kMaxNodePerms)
         return fail(CERAR_E_INVAL, "n_node_perms=%d outside [0, %d]", d->n_node_perms, kMaxNodePerms);
     if (d->n_node_perms > 0) {
@@ -561,6 +565,7 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
     p->info.proj_a0 = p->info.proj_b0 = kNaN;
     p->info.gamma = kNaN;
     p->info.h_choice = -1;
+    p->info.restart_used = -1;
     if (desc->svd_sweeps > 0) p->svd_sweeps = desc->svd_sweeps;
     int result = CERAR_OK;
     if (desc->kind == CERAR_VANDERMONDE) {
@@ -582,68 +587,96 @@ static int create_desc(const cerar_plan_desc *desc, cerar_plan **out) {
             if (eps * s.front() >= 1.0)
                 return fail(CERAR_E_INVAL, "eps ||H||_2 = %g must be < 1 (Sec. II-C)", eps * s.front());
         }
-        const int tries = desc->base ? 1 : 8;
-        for (int t = 0; t < tries; ++t) {
-            if (desc->base) {
-                p->B.assign(desc->base, desc->base + (size_t)N * c);
-                p->info.seed_used = 0;
-            } else {
-                p->B = gaussian_base(desc->seed + (uint64_t)t, N, c);
-                p->info.seed_used = desc->seed + (uint64_t)t;
+        // one construction from the seeds seed0, seed0 + 1, ... (a new B after
+        // an exactly singular window); KAPPA then runs the ALS from it
+        auto design = [&](uint64_t seed0) -> int {
+            std::vector<double> Hs = H;
+            int result = CERAR_OK;
+            const int tries = desc->base ? 1 : 8;
+            for (int t = 0; t < tries; ++t) {
+                if (desc->base) {
+                    p->B.assign(desc->base, desc->base + (size_t)N * c);
+                    p->info.seed_used = 0;
+                } else {
+                    p->B = gaussian_base(seed0 + (uint64_t)t, N, c);
+                    p->info.seed_used = seed0 + (uint64_t)t;
+                }
+                if (desc->n_node_perms > 0) {
+                    // the candidate H with the largest gamma for this B (Sec. II-C assumption)
+                    double best = -1.0;
+                    std::vector<double> Ht((size_t)c * c, 0.0);
+                    for (int q = 0; q < desc->n_node_perms; ++q) {
+                        const int *perm = desc->node_perms + (size_t)q * c;
+                        for (int j = 0; j < c; ++j) Ht[(size_t)j * c + j] = nodes[perm[j]];
+                        const double g = gamma_of(p, p->B, Ht, N, c);
+                        if (g > best) {
+                            best = g;
+                            Hs = Ht;
+                            p->info.h_choice = q;
+                        }
+                    }
+                    p->info.gamma = best;
+                } else {
+                    p->info.gamma = gamma_of(p, p->B, Hs, N, c);
+                }
+                p->D.assign((size_t)c * c, 0.0);
+                for (size_t a = 0; a < Hs.size(); ++a) p->D[a] = eps * Hs[a];
+                for (int j = 0; j < c; ++j) p->D[(size_t)j * c + j] += 1.0;
+                result = mpc_plan(p);
+                if (result != CERAR_E_SINGULAR) break;
             }
-            if (desc->n_node_perms > 0) {
-                // the candidate H with the largest gamma for this B (Sec. II-C assumption)
-                double best = -1.0;
-                std::vector<double> Ht((size_t)c * c, 0.0);
-                for (int q = 0; q < desc->n_node_perms; ++q) {
-                    const int *perm = desc->node_perms + (size_t)q * c;
-                    for (int j = 0; j < c; ++j) Ht[(size_t)j * c + j] = nodes[perm[j]];
-                    const double g = gamma_of(p, p->B, Ht, N, c);
-                    if (g > best) {
-                        best = g;
-                        H = Ht;
-                        p->info.h_choice = q;
+            if (result == CERAR_OK && desc->kind == CERAR_KAPPA) {
+                p->info.phi_initial = phi_of(p, p->U, p->R);
+                const int iters = desc->als_iters > 0 ? desc->als_iters : 100;
+                double a0 = kNaN, b0 = kNaN;
+                const bool project_first = desc->als_order == 1;
+                // the kappa guarantee rests on the projection's SVDs: one that
+                // did not converge fails the plan instead of weakening it
+                auto no_conv = [&] {
+                    return fail(CERAR_E_NOCONV, "one-sided Jacobi SVD of an encoder did not converge in %d sweeps "
+                                "(projection of Sec. II-D)", p->svd_sweeps);
+                };
+                for (int it = 0; it < iters && result == CERAR_OK; ++it) {
+                    if (!u_step(p, p->R, p->U)) {
+                        result = fail(CERAR_E_SINGULAR, "U-step normal equations singular");
+                    } else if (project_first) {             // U-step, projection, R-step
+                        if (!project(p, p->U, desc->param, a0, b0)) result = no_conv();
+                        else if (!r_step(p, p->U, p->R))
+                            result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
+                    } else {                                // U-step, R-step, projection (Sec. II-D)
+                        if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
+                        else if (!project(p, p->U, desc->param, a0, b0)) result = no_conv();
                     }
                 }
-                p->info.gamma = best;
-            } else {
-                p->info.gamma = gamma_of(p, p->B, H, N, c);
+                // the decoders of the final (projected) encoders
+                if (result == CERAR_OK && !project_first && !r_step(p, p->U, p->R))
+                    result = fail(CERAR_E_SINGULAR, "final R-step rank deficient");
+                p->info.proj_a0 = a0;
+                p->info.proj_b0 = b0;
+                p->D.clear();                                  // no closed form for the designed plan
             }
-            p->D.assign((size_t)c * c, 0.0);
-            for (size_t a = 0; a < H.size(); ++a) p->D[a] = eps * H[a];
-            for (int j = 0; j < c; ++j) p->D[(size_t)j * c + j] += 1.0;
-            result = mpc_plan(p);
-            if (result != CERAR_E_SINGULAR) break;
-        }
-        if (result == CERAR_OK && desc->kind == CERAR_KAPPA) {
-            p->info.phi_initial = phi_of(p, p->U, p->R);
-            const int iters = desc->als_iters > 0 ? desc->als_iters : 100;
-            double a0 = kNaN, b0 = kNaN;
-            const bool project_first = desc->als_order == 1;
-            // the kappa guarantee rests on the projection's SVDs: one that
-            // did not converge fails the plan instead of weakening it
-            auto no_conv = [&] {
-                return fail(CERAR_E_NOCONV, "one-sided Jacobi SVD of an encoder did not converge in %d sweeps "
-                            "(projection of Sec. II-D)", p->svd_sweeps);
-            };
-            for (int it = 0; it < iters && result == CERAR_OK; ++it) {
-                if (!u_step(p, p->R, p->U)) {
-                    result = fail(CERAR_E_SINGULAR, "U-step normal equations singular");
-                } else if (project_first) {             // U-step, projection, R-step
-                    if (!project(p, p->U, desc->param, a0, b0)) result = no_conv();
-                    else if (!r_step(p, p->U, p->R))
-                        result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
-                } else {                                // U-step, R-step, projection (Sec. II-D)
-                    if (!r_step(p, p->U, p->R)) result = fail(CERAR_E_SINGULAR, "R-step least squares rank deficient");
-                    else if (!project(p, p->U, desc->param, a0, b0)) result = no_conv();
-                }
+            return result;
+        };
+        result = design(desc->seed);
+        // KAPPA restarts (Sec. II-D's problem is nonconvex): the ALS from the
+        // O(eps0) plans of further random bases B, keeping the least Phi
+        const int restarts = desc->kind == CERAR_KAPPA && desc->als_restarts > 1 ? desc->als_restarts : 1;
+        if (desc->kind == CERAR_KAPPA && result == CERAR_OK) p->info.restart_used = 0;
+        for (int r = 1; r < restarts && result == CERAR_OK; ++r) {
+            const double best_phi = phi_of(p, p->U, p->R);
+            std::vector<double> bU = p->U, bR = p->R, bB = p->B;
+            const cerar_plan_info bI = p->info;
+            const int st = design(desc->seed + 8 * (uint64_t)r);
+            if (st == CERAR_OK && phi_of(p, p->U, p->R) < best_phi) {
+                p->info.restart_used = r;
+            } else {                                     // keep the best so far
+                p->U.swap(bU);
+                p->R.swap(bR);
+                p->B.swap(bB);
+                p->info = bI;
+                clear_error();
             }
-            // the decoders of the final (projected) encoders
-            if (result == CERAR_OK && !project_first && !r_step(p, p->U, p->R))
-                result = fail(CERAR_E_SINGULAR, "final R-step rank deficient");
-            p->info.proj_a0 = a0;
-            p->info.proj_b0 = b0;
-            p->D.clear();                                  // no closed form for the designed plan
+            p->D.clear();                                  // a failed restart may leave its O(eps0) D
         }
     }
     if (result == CERAR_OK) result = finish_plan(p, desc->kind, desc->param, out);
@@ -668,6 +701,7 @@ static int create_explicit(int N, int c, const double *U, const double *R, cerar
     p->info.proj_a0 = p->info.proj_b0 = kNaN;
     p->info.gamma = kNaN;
     p->info.h_choice = -1;
+    p->info.restart_used = -1;
     int result = finish_plan(p, CERAR_EXPLICIT, kNaN, out);
     if (result == CERAR_OK) holder.release();
     return result;

@@ -29,7 +29,7 @@ def header_functions():
 
 def test_library_exports_every_declared_function():
     names = header_functions()
-    assert len(names) == 21
+    assert len(names) == 22
     lib = C.lib()
     for n in names:
         assert hasattr(lib, n), n
@@ -376,3 +376,29 @@ def test_default_sweep_cap_suffices_for_the_workload_plans(N, c, kind, param):
     kw = {"als_iters": 3} if kind == "kappa" else {}
     plan = C.Plan(N, c, kind, param, seed=1000 + N, **kw)
     assert plan.info()["svd_converged"] == 1
+
+
+def test_als_restarts_keep_the_least_phi():
+    """KAPPA restarts (Sec. II-D: the problem is nonconvex): runs from the
+    O(eps0) plans of bases of seeds seed, seed + 8, ...; the kept plan has the
+    least Phi of them and still meets the kappa bound.  Each run equals a
+    plain plan of that seed."""
+    N, c, kmax, it = 4, 12, 60.0, 8
+    runs = [C.Plan(N, c, "kappa", kmax, seed=5 + 8 * r, als_iters=it, als_order=1) for r in range(3)]
+    phis = [pl.info()["phi"] for pl in runs]
+    best = C.Plan(N, c, "kappa", kmax, seed=5, als_iters=it, als_order=1, als_restarts=3)
+    info = best.info()
+    r = int(np.argmin(phis))
+    assert info["restart_used"] == r
+    assert info["phi"] == pytest.approx(min(phis), rel=1e-12)
+    np.testing.assert_array_equal(best.matrices()[0], runs[r].matrices()[0])
+    assert info["kappa_M"] <= kmax * (1 + 1e-9)
+    assert info["seed_used"] == runs[r].info()["seed_used"]
+    assert runs[0].info()["restart_used"] == 0
+    assert C.Plan(N, c, "o_eps", 0.1, seed=5).info()["restart_used"] == -1
+    with pytest.raises(C.CerarError) as ei:                # restarts draw new bases
+        C.Plan(N, c, "kappa", kmax, base=synth.base_matrix(1, N, c), als_restarts=2)
+    assert ei.value.status == -1
+    with pytest.raises(C.CerarError) as ei:
+        C.Plan(N, c, "kappa", kmax, seed=5, als_restarts=65)
+    assert ei.value.status == -1

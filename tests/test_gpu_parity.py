@@ -457,6 +457,32 @@ def test_error_norms_kernel():
     np.testing.assert_allclose(norms.cpu().numpy(), ref, rtol=1e-12)
 
 
+def test_sampled_norms_kernel():
+    """K5's parity term: squared differences against reference values at
+    sampled flat indices, and squared references, per worker in fp64; an
+    index outside [0, d) makes the sums NaN instead of reading out of range."""
+    torch, dev = torch_dev()
+    N, d, count = 5, 100_003, 5000
+    rng = np.random.default_rng(18)
+    o = host_grads(N, d, seed=18)
+    idx = rng.integers(0, d, size=count).astype(np.int64)
+    ref = rng.standard_normal((N, count))
+    norms = torch.empty(2 * N, dtype=torch.float64, device=dev)
+    out = to_device(o, ld=d + 3)
+    C.sampled_norms(N, d, torch.from_numpy(idx).to(dev), torch.from_numpy(ref).to(dev), out, norms)
+    sync()
+    got = norms.cpu().numpy()
+    for i in range(N):
+        g = o[i][idx].astype(np.float64)
+        np.testing.assert_allclose(got[2 * i], np.sum((g - ref[i]) ** 2), rtol=1e-12)
+        np.testing.assert_allclose(got[2 * i + 1], np.sum(ref[i] ** 2), rtol=1e-12)
+    idx[17] = d                                     # one index past the end
+    C.sampled_norms(N, d, torch.from_numpy(idx).to(dev), torch.from_numpy(ref).to(dev), out, norms)
+    sync()
+    got = norms.cpu().numpy()
+    assert np.all(np.isnan(got[0::2])) and np.all(np.isfinite(got[1::2]))
+
+
 def test_bucketed_matches_independent_instances():
     torch, dev = torch_dev()
     N, c = 4, 8

@@ -97,6 +97,14 @@ def check_sampled(name, wl, U, R, grads, out, pos, kappa, gated=True, off=0, len
     refv = [r[valid] for r in ref]
     S = sum(g[valid] for g in G)
     parity = max(per_worker_rel(gpu, refv))
+    # the same term from K5 on the device (cerar_sampled_norms)
+    torch, dev = torch_dev()
+    nrm = torch.empty(2 * wl.N, dtype=torch.float64, device=dev)
+    C.sampled_norms(wl.N, off + length, torch.from_numpy(np.ascontiguousarray(sel, dtype=np.int64)).to(dev),
+                    torch.from_numpy(np.ascontiguousarray(np.stack(refv))).to(dev), out, nrm)
+    nm = nrm.cpu().numpy()
+    parity_k5 = max(float(np.sqrt(nm[2 * i] / nm[2 * i + 1])) for i in range(wl.N))
+    assert abs(parity_k5 - parity) <= 1e-9 * parity + 1e-15, (parity_k5, parity)
     err_gpu = max(per_worker_rel(gpu, [S] * wl.N))
     err_orc = max(per_worker_rel(refv, [S] * wl.N))
     print(f"{name}: {len(pos)} positions, kappa_M={kappa:.3g} parity={parity:.3g} "
