@@ -543,10 +543,10 @@ __device__ __forceinline__ void k_encode_dbuf_body(const EncParams &a, unsigned 
 }
 
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_dbuf(EncParams a) { k_encode_dbuf_body<KS, MTC>(a, blockIdx.x); }
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 4 : 2, MTC <= 2 ? 4 : 2))) void k_encode_dbuf(EncParams a) { k_encode_dbuf_body<KS, MTC>(a, blockIdx.x); }
 
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_dbuf_batch(EncBatch b) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 4 : 2, MTC <= 2 ? 4 : 2))) void k_encode_dbuf_batch(EncBatch b) {
     unsigned bid;
     const EncParams a = b.at(bid);
     k_encode_dbuf_body<KS, MTC>(a, bid);
@@ -911,10 +911,10 @@ __device__ __forceinline__ void k_decode_dbuf_body(const DecParams &a, unsigned 
 }
 
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_dbuf(DecParams a) { k_decode_dbuf_body<KS, MTC>(a, blockIdx.x); }
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 3 : 2, MTC <= 2 ? 3 : 2))) void k_decode_dbuf(DecParams a) { k_decode_dbuf_body<KS, MTC>(a, blockIdx.x); }
 
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_dbuf_batch(DecBatch b) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 3 : 2, MTC <= 2 ? 3 : 2))) void k_decode_dbuf_batch(DecBatch b) {
     unsigned bid;
     const DecParams a = b.at(bid);
     k_decode_dbuf_body<KS, MTC>(a, bid);
@@ -1644,6 +1644,12 @@ void launch_encode_ks(const P &a, Path path, size_t lds, hipStream_t s, dim3 gri
                     return;
                 }
             }
+            if constexpr (KS == 8) {
+                if (sh.MT == 2 && sh.mt0 == 0 && sh.mt1 == 2) {   // c = 32: double-buffered
+                    go_encode_dbuf<KS, 2>(a, grid, (size_t)2 * (KS / 4) * 256 * sizeof(float), s);
+                    return;
+                }
+            }
             // up to 4 M-tiles: the pipelined kernel, coefficients staged in LDS;
             // NB blocks per wave keep ~16 KB of loads in flight per wave at any c
             constexpr int MTMAX = KS <= 4 ? 1 : (KS <= 8 ? 2 : 4);
@@ -1668,6 +1674,13 @@ void launch_decode_ks(const P &a, Path path, size_t lds, hipStream_t s, dim3 gri
     if constexpr (KS == 18 || KS == 20) {                // c = 64: K = 63 + N >= 65 observations
         if (path == Path::kFast && sh.MT == 4 && sh.mt0 == 0 && sh.mt1 == 4) {   // double-buffered
             go_decode_dbuf<KS, 4>(a, grid, (size_t)4 * ((KS + 3) / 4) * 256 * sizeof(float) +
+                                               (size_t)4 * KS * sizeof(float *), s);
+            return;
+        }
+    }
+    if constexpr (KS == 10 || KS == 12) {                // c = 32: K = 31 + N, N <= 17
+        if (path == Path::kFast && sh.MT == 2 && sh.mt0 == 0 && sh.mt1 == 2) {   // double-buffered
+            go_decode_dbuf<KS, 2>(a, grid, (size_t)2 * ((KS + 3) / 4) * 256 * sizeof(float) +
                                                (size_t)4 * KS * sizeof(float *), s);
             return;
         }

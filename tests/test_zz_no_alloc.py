@@ -85,3 +85,36 @@ def test_noalloc_limits_and_preconditions():
     C.ring_simulate_noalloc(fresh, big_ok, g, work2, out2)
     torch.cuda.synchronize()
     assert bool(torch.equal(out, out2))
+
+
+def test_noalloc_records_into_a_graph():
+    """The callers it serves include code under HIP graph capture: after
+    cerar_plan_prepare_device the call allocates nothing and only launches
+    kernels, so it is recorded with no eager call first.  Each replay, on
+    fresh inputs copied into the captured buffers and with eager calls and a
+    synchronisation in between, equals cerar_ring_simulate on those inputs."""
+    torch, dev = torch_dev()
+    N, c, d = 8, 32, 32 * 2048 + 7
+    U, R = orthogonal_plan(N, c, seed=75)
+    plan = C.Plan.explicit(U, R)
+    plan.prepare_device()
+    grads = torch.zeros((N, d), dtype=torch.float32, device=dev)
+    work, _, out = buffers(plan, d)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        C.ring_simulate_noalloc(plan, d, grads, work, out)
+    torch.cuda.synchronize()
+    for r in range(3):
+        g = host_grads(N, d, seed=750 + r)
+        grads.copy_(torch.from_numpy(g).to(dev))
+        out.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        gref = to_device(g)
+        wref, wsref, oref = buffers(plan, d)
+        C.ring_simulate(plan, d, gref, wref, wsref, oref)
+        torch.cuda.synchronize()
+        assert bool(torch.equal(out, oref)), f"replay {r}"
+        if r == 0:
+            assert max_rel_l2(out.double().cpu().numpy(), oracle_allreduce(g, U, R)) <= 1e-4
+    del graph
