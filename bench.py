@@ -584,6 +584,8 @@ def main():
     for name, key in (("k_encode (K1)", "encode"), ("k_decode (K4)", "decode")):
         kernels[name]["tflops"] = N * flops[key] / (kernels[name]["avg_ms"] * 1e-3) / 1e12
         kernels[name]["mfma_frac"] = kernels[name]["tflops"] / FP32_MFMA_PEAK_TFLOPS
+    for name in kernels:                            # every family against the HBM peak
+        kernels[name]["hbm_frac"] = kernels[name]["gbps"] / HBM_PEAK_GBS
     # per-step spans (first event to last) of the timed loop: the paper reports
     # the median over runs (appendix, details of the numerical experiments);
     # the value above is the mean over the timed steps
