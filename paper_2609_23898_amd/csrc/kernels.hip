@@ -486,7 +486,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 // it: the compiler's wait counts at the header merge the prologue with the
 // back edge, and a header before the first tile made every other block wait
 // for all of the previous block's stores to drain.
-template <int KS, int MTC>
+template <int KS, int MTC, bool ROT>
 __device__ __forceinline__ void k_encode_dbuf_body(const EncParams &a, unsigned bid) {
     extern __shared__ float sfrag[];
     const int worker = bid % a.N;           // workers interleaved across the grid
@@ -501,7 +501,13 @@ __device__ __forceinline__ void k_encode_dbuf_body(const EncParams &a, unsigned 
     float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
     float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
     const size_t p = a.sb.p;
-    const size_t first = a.blk0 + (size_t)wg * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
+    // ROT: worker w's runs of blocks start w/N of the row further on
+    // (wrapping), so the workers do not sweep the same positions at the
+    // same time (in-process A/B at N = 8, c = 64: encode 0.6 % faster, decode
+    // equal or up to 6 % faster).  A single instance only: a batch's
+    // instances have their own workgroup counts.
+    const int wgr = ROT ? (wg + worker * (a.wg_per_worker / a.N)) % a.wg_per_worker : wg;
+    const size_t first = a.blk0 + (size_t)wgr * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
     size_t blk = first + wave;
     if (blk >= end) return;
     v4f b0[KS], b1[KS];
@@ -543,13 +549,13 @@ __device__ __forceinline__ void k_encode_dbuf_body(const EncParams &a, unsigned 
 }
 
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 4 : 2, MTC <= 2 ? 4 : 2))) void k_encode_dbuf(EncParams a) { k_encode_dbuf_body<KS, MTC>(a, blockIdx.x); }
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 4 : 2, MTC <= 2 ? 4 : 2))) void k_encode_dbuf(EncParams a) { k_encode_dbuf_body<KS, MTC, true>(a, blockIdx.x); }
 
 template <int KS, int MTC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 4 : 2, MTC <= 2 ? 4 : 2))) void k_encode_dbuf_batch(EncBatch b) {
     unsigned bid;
     const EncParams a = b.at(bid);
-    k_encode_dbuf_body<KS, MTC>(a, bid);
+    k_encode_dbuf_body<KS, MTC, false>(a, bid);
 }
 
 // ---- K2/K3: one ring round ---------------------------------------------------
@@ -852,7 +858,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(KS * N
 // Double-buffered interior decode for c = 16 MTC (up to 64), same scheme as
 // the double-buffered encode; the B rows come through the per-worker table of
 // observation slots.
-template <int KS, int MTC>
+template <int KS, int MTC, bool ROT>
 __device__ __forceinline__ void k_decode_dbuf_body(const DecParams &a, unsigned bid) {
     extern __shared__ float smem[];
     const int worker = bid % a.N;           // workers interleaved across the grid
@@ -870,7 +876,13 @@ __device__ __forceinline__ void k_decode_dbuf_body(const DecParams &a, unsigned 
     __syncthreads();
     float *out = a.out + (size_t)worker * a.ld_o;
     const size_t p = a.sb.p;
-    const size_t first = a.blk0 + (size_t)wg * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
+    // ROT: worker w's runs of blocks start w/N of the row further on
+    // (wrapping), so the workers do not sweep the same positions at the
+    // same time (in-process A/B at N = 8, c = 64: encode 0.6 % faster, decode
+    // equal or up to 6 % faster).  A single instance only: a batch's
+    // instances have their own workgroup counts.
+    const int wgr = ROT ? (wg + worker * (a.wg_per_worker / a.N)) % a.wg_per_worker : wg;
+    const size_t first = a.blk0 + (size_t)wgr * a.blk_per_wg, end = min(a.blk1, first + a.blk_per_wg);
     size_t blk = first + wave;
     if (blk >= end) return;
     v4f b0[KS], b1[KS];
@@ -911,13 +923,13 @@ __device__ __forceinline__ void k_decode_dbuf_body(const DecParams &a, unsigned 
 }
 
 template <int KS, int MTC>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 3 : 2, MTC <= 2 ? 3 : 2))) void k_decode_dbuf(DecParams a) { k_decode_dbuf_body<KS, MTC>(a, blockIdx.x); }
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 3 : 2, MTC <= 2 ? 3 : 2))) void k_decode_dbuf(DecParams a) { k_decode_dbuf_body<KS, MTC, true>(a, blockIdx.x); }
 
 template <int KS, int MTC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <= 2 ? 3 : 2, MTC <= 2 ? 3 : 2))) void k_decode_dbuf_batch(DecBatch b) {
     unsigned bid;
     const DecParams a = b.at(bid);
-    k_decode_dbuf_body<KS, MTC>(a, bid);
+    k_decode_dbuf_body<KS, MTC, false>(a, bid);
 }
 
 // Wide decode for c = 16 MTC > 64 with more observations than the
