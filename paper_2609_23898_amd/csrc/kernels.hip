@@ -134,6 +134,11 @@ __device__ inline uint32_t opaque(uint32_t x) {
     asm volatile("" : "+v"(x));
     return x;
 }
+// The same for a wave-uniform value (kept in scalar registers).
+__device__ inline size_t opaque_s(size_t x) {
+    asm volatile("" : "+s"(x));
+    return x;
+}
 // The encode reads the gradient with ordinary loads: measured faster than
 // streaming loads for its c-row access pattern (the decode and the rounds
 // stream with non-temporal loads, which measured faster for them).
@@ -932,9 +937,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(MTC <=
     k_decode_dbuf_body<KS, MTC, false>(a, bid);
 }
 
-// Wide decode for c = 16 MTC > 64 with more observations than the
-// four-wave kernel below holds in LDS twice per CU (K > 144): at 2(L+1)c
-// flops per position the contraction is bound by the fp32 MFMA rate, so one
+// Wide decode for c = 16 MTC > 64 with more observations (K > 144) than the
+// split-operand kernel below takes: at 2(L+1)c flops per position the
+// contraction is bound by the fp32 MFMA rate, so one
 // wave per SIMD runs it with two register buffers of B operands: half-block
 // n+1's loads are in flight while half-block n's MTC M-tiles run, and each
 // tile's 16 output rows are stored as soon as it is done.  Half-blocks of 32
@@ -1005,99 +1010,338 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     }
 }
 
-// c = 128 with four waves per SIMD (measured 11 % faster for the encode and
-// 6 % for the decode than one double-buffered wave per SIMD, which leaves
-// nothing to cover a wave's own waits).  512-thread workgroups
-// (8 waves) share one LDS copy of the coefficient fragments (64 KiB for the
-// encode, 72 KiB for the decode at K <= 144), two workgroups fit a CU, and
-// each wave keeps a single buffer of B operands within 128 registers: while
-// one wave waits for its half-block's loads, the other waves on its SIMD
-// keep the MFMA pipe busy.
-constexpr int kWideWaves = 8;
+// ---- c = 128: the contraction on bf16 MFMAs at fp32 accuracy -----------------
+// At c = 128 the encode and decode do 32 flop per algorithmic byte, and the
+// fp32 MFMA rate bounds them: with the contraction taken out, the same loads
+// and stores take two thirds of the time.  Here every fp32 operand x is
+// split exactly into three bf16 terms, x = h + m + l: h is x rounded to bf16
+// (round to nearest even), m the remainder rounded to bf16, l the rest, which
+// bf16 holds exactly (8 significant bits).  Of the nine products of two split
+// operands the six with h h, h m, m h, h l, m m, l h are kept; each is exact
+// in fp32, and since |m| <= 2^-8 |x| (1 + 2^-8) and |l| <= 2^-16 |x|, the
+// dropped m l, l m and l l sum to less than 2^-23 |a||b|, two units of fp32
+// rounding, so a product is fp32-accurate (the six-product scheme of Henry, Tang
+// and Heinecke, "Leveraging the bfloat16 artificial intelligence datatype
+// for higher-precision computations", ARITH 2019).  The 16x16x32 bf16 MFMA
+// does 32 K-steps in half the cycles the fp32 one takes for 4, so the six
+// products cost 3/8 of the fp32 MFMA time.  Values must lie in bf16's range
+// (|x| < 3.39e38); terms below fp32's normal range lose their low bits.
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef __bf16 v4bf __attribute__((ext_vector_type(4)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 
-template <int KS, int MTC>
-__global__ __launch_bounds__(64 * kWideWaves) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_encode_wide_sb(EncParams a) {
+constexpr int kSplitWaves = 8;                 // 512-thread workgroups, one per CU (LDS)
+constexpr int kSplitKC = 4;                    // c = 128: four chunks of 32 K-steps
+
+__device__ inline void split3(float x, __bf16 &h, __bf16 &m, __bf16 &l) {
+    h = (__bf16)x;
+    const float r = x - (float)h;                 // exact
+    m = (__bf16)r;
+    l = (__bf16)(r - (float)m);                   // exact
+}
+
+template <class V>
+struct Split3 { V h, m, l; };
+
+// acc += A B for split A and B with the six kept products, the small ones first.
+__device__ inline v4f mma_split32(const Split3<v8bf> &a, const Split3<v8bf> &b, v4f acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.l, b.h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.m, b.m, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.h, b.l, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.m, b.h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.h, b.m, acc, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.h, b.h, acc, 0, 0, 0);
+}
+__device__ inline v4s as_v4s(v4bf v) { return __builtin_bit_cast(v4s, v); }
+__device__ inline v4f mma_split16(const Split3<v4bf> &a, const Split3<v4bf> &b, v4f acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_v4s(a.l), as_v4s(b.h), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_v4s(a.m), as_v4s(b.m), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_v4s(a.h), as_v4s(b.l), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_v4s(a.m), as_v4s(b.h), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_v4s(a.h), as_v4s(b.m), acc, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(as_v4s(a.h), as_v4s(b.h), acc, 0, 0, 0);
+}
+
+// The A operands in LDS, split: for M-tile mt and 32-step chunk kc, the
+// three terms of lane l are 8 bf16 at [((mt KC + kc) 3 + term) 64 + l] x 16 B,
+// holding A[row 16 mt + l % 16][k = 32 kc + 8 (l / 16) + s], s = 0..7; a
+// 16-step tail (decode) follows at [(mt 3 + term) 64 + l] x 8 B with
+// k = 32 KC + 4 (l / 16) + s, s = 0..3.  The fp32 fragment of (row, k) is
+// gfrag[((mt KSx + k / 4) 64 + 16 (k % 4) + row % 16], zero beyond 4 KSx.
+template <int MTC, int KC, bool TAIL>
+__device__ inline void stage_split_fragments(__bf16 *sa, const float *gfrag, int KSx) {
+    constexpr int KT = 32 * KC + (TAIL ? 16 : 0);
+    auto coef = [&](int mt, int row, int k) {
+        return k < 4 * KSx ? gfrag[((size_t)mt * KSx + k / 4) * 64 + 16 * (k % 4) + row] : 0.0f;
+    };
+    for (int idx = threadIdx.x; idx < MTC * KT * 16; idx += 64 * kSplitWaves) {
+        const int mt = idx / (KT * 16), rem = idx % (KT * 16);
+        if (rem < 32 * KC * 16) {
+            const int s = rem & 7, lane = (rem >> 3) & 63, kc = rem >> 9;
+            const int row = lane & 15, k = 32 * kc + 8 * (lane >> 4) + s;
+            __bf16 *base = sa + (((size_t)(mt * KC + kc) * 3) * 64 + lane) * 8 + s;
+            split3(coef(mt, row, k), base[0], base[64 * 8], base[2 * 64 * 8]);
+        } else {
+            const int r2 = rem - 32 * KC * 16;
+            const int s = r2 & 3, lane = r2 >> 2;
+            const int row = lane & 15, k = 32 * KC + 4 * (lane >> 4) + s;
+            __bf16 *base = sa + (size_t)MTC * KC * 3 * 64 * 8 + ((size_t)(mt * 3) * 64 + lane) * 4 + s;
+            split3(coef(mt, row, k), base[0], base[64 * 4], base[2 * 64 * 4]);
+        }
+    }
+}
+
+template <int MTC, int KC>
+__device__ inline Split3<v8bf> lds_split32(const __bf16 *sa, int mt, int kc, uint32_t lane8) {
+    const __bf16 *b = sa + ((size_t)(mt * KC + kc) * 3) * 64 * 8 + lane8;
+    return {*reinterpret_cast<const v8bf *>(b), *reinterpret_cast<const v8bf *>(b + 64 * 8),
+            *reinterpret_cast<const v8bf *>(b + 2 * 64 * 8)};
+}
+template <int MTC, int KC>
+__device__ inline Split3<v4bf> lds_split16(const __bf16 *sa, int mt, uint32_t lane4) {
+    const __bf16 *b = sa + (size_t)MTC * KC * 3 * 64 * 8 + (size_t)(mt * 3) * 64 * 4 + lane4;
+    return {*reinterpret_cast<const v4bf *>(b), *reinterpret_cast<const v4bf *>(b + 64 * 4),
+            *reinterpret_cast<const v4bf *>(b + 2 * 64 * 4)};
+}
+
+// One half-block (32 positions) of B operands, split: lane (col, g) holds rows
+// 32 kc + 8 g + s (s = 0..7) and 32 KC + 4 g + s (tail, s = 0..3) at
+// positions 2 col and 2 col + 1 (component q).
+template <int KC, bool TAIL>
+struct SplitB {
+    Split3<v8bf> b[KC][2];
+    Split3<v4bf> t[2];
+};
+
+// Two values at once (one packed conversion per term); returns the three
+// terms as packed bf16 pairs.
+__device__ inline void split3_pair(v2f x, uint32_t &h, uint32_t &m, uint32_t &l) {
+    const v2bf xh = __builtin_convertvector(x, v2bf);
+    const v2f r = x - __builtin_convertvector(xh, v2f);        // exact
+    const v2bf xm = __builtin_convertvector(r, v2bf);
+    const v2bf xl = __builtin_convertvector(r - __builtin_convertvector(xm, v2f), v2bf);   // exact
+    h = __builtin_bit_cast(uint32_t, xh);
+    m = __builtin_bit_cast(uint32_t, xm);
+    l = __builtin_bit_cast(uint32_t, xl);
+}
+
+template <int KC, bool TAIL>
+__device__ inline void split_operands(SplitB<KC, TAIL> &S, const v2f (&x)[KC][8], const v2f (&xt)[4]) {
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            v4u h, m, l;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t th, tm, tl;
+                split3_pair(v2f{x[kc][2 * w][q], x[kc][2 * w + 1][q]}, th, tm, tl);
+                h[w] = th;
+                m[w] = tm;
+                l[w] = tl;
+            }
+            S.b[kc][q] = {__builtin_bit_cast(v8bf, h), __builtin_bit_cast(v8bf, m), __builtin_bit_cast(v8bf, l)};
+        }
+    if constexpr (TAIL)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            v2u h, m, l;
+#pragma unroll
+            for (int w = 0; w < 2; ++w) {
+                uint32_t th, tm, tl;
+                split3_pair(v2f{xt[2 * w][q], xt[2 * w + 1][q]}, th, tm, tl);
+                h[w] = th;
+                m[w] = tm;
+                l[w] = tl;
+            }
+            S.t[q] = {__builtin_bit_cast(v4bf, h), __builtin_bit_cast(v4bf, m), __builtin_bit_cast(v4bf, l)};
+        }
+}
+
+// M-tiles mt and mt + 1 of one half-block: four independent MFMA chains.
+// The LDS offsets come through opaque(), so that the coefficient loads,
+// which do not change from one half-block to the next, are not hoisted out
+// of the block loop (all of them would not fit the registers).
+template <int MTC, int KC, bool TAIL>
+__device__ inline void mtile2_split(v4f (&acc)[2][2], const SplitB<KC, TAIL> &S, const __bf16 *sa, int mt, int lane) {
+    const uint32_t lane8 = opaque((uint32_t)lane * 8), lane4 = (uint32_t)lane * 4;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) acc[m][0] = acc[m][1] = v4f{0.f, 0.f, 0.f, 0.f};
+    // one chunk's coefficients in flight ahead of the MFMAs; the scheduling
+    // barriers keep the compiler from issuing more of them earlier
+    Split3<v8bf> a0 = lds_split32<MTC, KC>(sa, mt, 0, lane8), a1 = lds_split32<MTC, KC>(sa, mt + 1, 0, lane8);
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+        Split3<v8bf> n0 = a0, n1 = a1;
+        if (kc + 1 < KC) {
+            n0 = lds_split32<MTC, KC>(sa, mt, kc + 1, lane8);
+            n1 = lds_split32<MTC, KC>(sa, mt + 1, kc + 1, lane8);
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            acc[0][q] = mma_split32(a0, S.b[kc][q], acc[0][q]);
+            acc[1][q] = mma_split32(a1, S.b[kc][q], acc[1][q]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        a0 = n0;
+        a1 = n1;
+    }
+    if constexpr (TAIL) {
+        const uint32_t l4 = opaque(lane4);
+        const Split3<v4bf> a0 = lds_split16<MTC, KC>(sa, mt, l4), a1 = lds_split16<MTC, KC>(sa, mt + 1, l4);
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            acc[0][q] = mma_split16(a0, S.t[q], acc[0][q]);
+            acc[1][q] = mma_split16(a1, S.t[q], acc[1][q]);
+        }
+    }
+}
+
+// Encode at c = 128 on split operands.  Each wave splits its half-block's 128
+// rows once into registers, issues the next half-block's loads into the fp32
+// registers that just became free, and then runs the 8 M-tiles.  The loop
+// header sits after the split, where on every path the last vector-memory
+// operations issued are those loads, so waiting for them never drains the
+// stores of the half-block before.
+template <int MTC>
+__global__ __launch_bounds__(64 * kSplitWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_encode_split(EncParams a) {
     static_assert(MTC % 2 == 0, "M-tiles run in pairs");
-    extern __shared__ float sfrag[];
+    constexpr int KC = kSplitKC;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __bf16 *sa = reinterpret_cast<__bf16 *>(smem_raw);
     const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
     const int wg = blockIdx.x / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int col = lane & 15, krow = lane >> 4;
-    const int KSx = a.KSe;
-    constexpr int Q = (KS + 3) / 4;
-    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS, 64 * kWideWaves);
+    const int col = lane & 15, g = lane >> 4;
+    stage_split_fragments<MTC, KC, false>(sa, a.frag + (size_t)worker * a.MT * a.KSe * 64, a.KSe);
     __syncthreads();
     const float *src = a.grads + (size_t)worker * a.ld_g;
     float *dst = a.sb.work + (size_t)worker * a.sb.ld_work;
     float *x1 = a.sb.pool + (size_t)worker * a.N * a.sb.pool_stride;
     const size_t p = a.sb.p;
-    // half-blocks of 32 positions: [2 blk0, 2 blk1)
     const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
                  end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
-    for (size_t hb = first + wave; hb < end; hb += kWideWaves) {
-        v2f b[KS];
-        const uint32_t lane_in = opaque((uint32_t)(((size_t)krow * p + 2 * (size_t)col) * sizeof(float)));
+    size_t hb = first + wave;
+    if (hb >= end) return;
+    const uint32_t lane_in = opaque((uint32_t)(((size_t)(8 * g) * p + 2 * (size_t)col) * sizeof(float)));
+    v2f x[KC][8], xt[4];
+    // the row offsets are recomputed from a laundered stride in every
+    // half-block: held across the loop, 64 of them would not fit the scalar
+    // registers
+    auto load = [&](size_t h) {
+        const size_t ps = opaque_s(p);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) b[ks] = load2_off(src + hb * 32 + (size_t)(4 * min(ks, KSx - 1)) * p, lane_in);
+        for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+            for (int s = 0; s < 8; ++s) x[kc][s] = load2_off(src + h * 32 + (size_t)(32 * kc + s) * ps, lane_in);
+    };
+    SplitB<KC, false> S;
+    load(hb);
+    split_operands<KC, false>(S, x, xt);
+    size_t next = hb + kSplitWaves;
+    if (next < end) load(next);
+    while (true) {
         const size_t e0 = hb * 32;
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(g * 4) * p + 2 * (size_t)col) * sizeof(float)));
 #pragma unroll
-        for (int mt = 0; mt < MTC; mt += 2) {        // M-tiles mt and mt + 1
-            const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
+        for (int mt = 0; mt < MTC; mt += 2) {
             v4f acc[2][2];
-            mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
+            mtile2_split<MTC, KC, false>(acc, S, sa, mt, lane);
+            const size_t ps = opaque_s(p);
 #pragma unroll
             for (int m = 0; m < 2; ++m)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const v2f v = {acc[m][0][r], acc[m][1][r]};
-                    nt_store2_off(dst + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
-                    if (mt + m == 0 && krow * 4 + r == 0) nt_store2_off(x1 + e0, (uint32_t)(2 * col * sizeof(float)), v);
+                    nt_store2_off(dst + e0 + (size_t)((mt + m) * 16 + r) * ps, lane_out, v);
+                    if (mt + m == 0 && g * 4 + r == 0) nt_store2_off(x1 + e0, (uint32_t)(2 * col * sizeof(float)), v);
                 }
         }
+        if (next >= end) break;
+        hb = next;
+        split_operands<KC, false>(S, x, xt);
+        __builtin_amdgcn_sched_barrier(0);
+        next = hb + kSplitWaves;
+        if (next < end) load(next);
     }
 }
 
-template <int KS, int MTC>
-__global__ __launch_bounds__(64 * kWideWaves) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_decode_wide_sb(DecParams a) {
+// Decode at c = 128 (K = L + 1 <= 144 observations: four 32-step chunks and a
+// 16-step tail) on split operands, in the same order as k_encode_split.
+template <int MTC>
+__global__ __launch_bounds__(64 * kSplitWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_decode_split(DecParams a) {
     static_assert(MTC % 2 == 0, "M-tiles run in pairs");
-    extern __shared__ float smem[];
+    constexpr int KC = kSplitKC, KROWS = 32 * KC + 16;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __bf16 *sa = reinterpret_cast<__bf16 *>(smem_raw);
+    const float **srow = reinterpret_cast<const float **>(smem_raw + (size_t)MTC * (KC * 3 * 64 * 8 + 3 * 64 * 4) * 2);
     const int worker = blockIdx.x % a.N;           // workers interleaved across the grid
     const int wg = blockIdx.x / a.N;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int col = lane & 15, krow = lane >> 4;
-    const int KSx = a.KSd;
-    constexpr int Q = (KS + 3) / 4;
-    float *sfrag = smem;
-    const float **srow = reinterpret_cast<const float **>(smem + (size_t)MTC * Q * 256);
-    stage_fragments_padded(sfrag, a.frag + (size_t)worker * a.MT * KSx * 64, MTC, KSx, KS, 64 * kWideWaves);
-    // rows K..4 KS-1 repeat row K-1, whose coefficients there are zero
-    for (int t = threadIdx.x; t < 4 * KS; t += 64 * kWideWaves)
+    const int col = lane & 15, g = lane >> 4;
+    stage_split_fragments<MTC, KC, true>(sa, a.frag + (size_t)worker * a.MT * a.KSd * 64, a.KSd);
+    // rows K..KROWS-1 repeat row K-1, whose coefficients there are zero
+    for (int t = threadIdx.x; t < KROWS; t += 64 * kSplitWaves)
         srow[t] = a.sb.ptr(a.ycols[(size_t)worker * a.K + min(t, a.K - 1)]);
     __syncthreads();
     float *out = a.out + (size_t)worker * a.ld_o;
     const size_t p = a.sb.p;
     const size_t first = 2 * (a.blk0 + (size_t)wg * a.blk_per_wg),
                  end = 2 * min(a.blk1, a.blk0 + ((size_t)wg + 1) * a.blk_per_wg);
-    for (size_t hb = first + wave; hb < end; hb += kWideWaves) {
-        v2f b[KS];
+    size_t hb = first + wave;
+    if (hb >= end) return;
+    v2f x[KC][8], xt[4];
+    // the row pointers are read from LDS in every half-block (laundered
+    // index): held across the loop, 36 per lane would not fit the registers
+    auto load = [&](size_t h) {
+        const float *const *r8 = srow + opaque((uint32_t)(8 * g));
+        const float *const *r4 = srow + 32 * KC + opaque((uint32_t)(4 * g));
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) b[ks] = nt_load2_g(srow[ks * 4 + krow] + hb * 32 + 2 * col);
+        for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+            for (int s = 0; s < 8; ++s) x[kc][s] = nt_load2_g(r8[32 * kc + s] + h * 32 + 2 * col);
+            __builtin_amdgcn_sched_barrier(0);        // a chunk's row pointers at a time
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) xt[s] = nt_load2_g(r4[s] + h * 32 + 2 * col);
+    };
+    SplitB<KC, true> S;
+    load(hb);
+    split_operands<KC, true>(S, x, xt);
+    size_t next = hb + kSplitWaves;
+    if (next < end) load(next);
+    while (true) {
         const size_t e0 = hb * 32;
+        const uint32_t lane_out = opaque((uint32_t)(((size_t)(g * 4) * p + 2 * (size_t)col) * sizeof(float)));
 #pragma unroll
-        for (int mt = 0; mt < MTC; mt += 2) {        // M-tiles mt and mt + 1
-            const uint32_t lane_out = opaque((uint32_t)(((size_t)(krow * 4) * p + 2 * (size_t)col) * sizeof(float)));
+        for (int mt = 0; mt < MTC; mt += 2) {
             v4f acc[2][2];
-            mtile2_mma_lds2<KS>(acc, b, sfrag + (size_t)mt * Q * 256, sfrag + (size_t)(mt + 1) * Q * 256, lane);
+            mtile2_split<MTC, KC, true>(acc, S, sa, mt, lane);
+            const size_t ps = opaque_s(p);
 #pragma unroll
             for (int m = 0; m < 2; ++m)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const v2f v = {acc[m][0][r], acc[m][1][r]};
-                    nt_store2_off(out + e0 + (size_t)((mt + m) * 16 + r) * p, lane_out, v);
+                    nt_store2_off(out + e0 + (size_t)((mt + m) * 16 + r) * ps, lane_out, v);
                 }
         }
+        if (next >= end) break;
+        hb = next;
+        split_operands<KC, true>(S, x, xt);
+        __builtin_amdgcn_sched_barrier(0);
+        next = hb + kSplitWaves;
+        if (next < end) load(next);
     }
 }
+
+// LDS of the split kernels: the split A operands, then (decode) the row table.
+constexpr size_t kSplitEncLds = (size_t)8 * kSplitKC * 3 * 64 * 8 * sizeof(__bf16);
+constexpr size_t kSplitDecLds = (size_t)8 * (kSplitKC * 3 * 64 * 8 + 3 * 64 * 4) * sizeof(__bf16) +
+                                (size_t)(32 * kSplitKC + 16) * sizeof(float *);
 
 // ---- single-GPU fused variant (not the counted path) ---------------------------
 // The whole all-reduce for one 64-position block of every worker in one
@@ -1600,6 +1844,16 @@ void wg_for(size_t nblk, int &wg_per_worker, size_t &blk_per_wg) {
     blk_per_wg = (nblk + w * kWaves - 1) / (w * kWaves) * kWaves;
 }
 
+// Workgroups of the c = 128 split kernels: one fits a CU (LDS), so each
+// worker gets about 1024 / N of them, about four per CU in all, and each
+// stages its split coefficients once for a long run of blocks.
+void wg_for_split(size_t nblk, int N, int &wg_per_worker, size_t &blk_per_wg) {
+    size_t w = std::max<size_t>(1, (1024 + (size_t)N - 1) / (size_t)N);
+    w = std::min(w, std::max<size_t>(1, (nblk + kWaves - 1) / kWaves));
+    blk_per_wg = (nblk + w * kWaves - 1) / (w * kWaves) * kWaves;
+    wg_per_worker = (int)((nblk + blk_per_wg - 1) / blk_per_wg);
+}
+
 // Launch flavours: interior blocks (FAST), masked 16-byte layout, scalar layout.
 enum class Path { kFast, kMaskedVec, kScalar };
 
@@ -1834,9 +2088,9 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
             EncParams w = a;
             w.blk0 = 0;
             w.blk1 = bs.interior;
-            wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
-            hipLaunchKernelGGL((k_encode_wide_sb<32, 8>), dim3((unsigned)(N * w.wg_per_worker)),
-                               dim3(64 * kWideWaves), (size_t)8 * 8 * 256 * sizeof(float), s, w);
+            wg_for_split(bs.interior, N, w.wg_per_worker, w.blk_per_wg);
+            hipLaunchKernelGGL((k_encode_split<8>), dim3((unsigned)(N * w.wg_per_worker)), dim3(64 * kSplitWaves),
+                               kSplitEncLds, s, w);
             if (bs.total > bs.interior) {
                 EncParams t = a;
                 t.blk0 = bs.interior;
@@ -1919,10 +2173,11 @@ int enqueue_decode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
         w.mt1 = 8;
         w.blk0 = 0;
         w.blk1 = bs.interior;
-        wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
+        if (ks <= 36) wg_for_split(bs.interior, N, w.wg_per_worker, w.blk_per_wg);
+        else wg_for(bs.interior, w.wg_per_worker, w.blk_per_wg);
         const dim3 grid((unsigned)(N * w.wg_per_worker));
         auto lds_for = [](int K4) { return (size_t)8 * (K4 / 4) * 256 * sizeof(float) + (size_t)4 * K4 * sizeof(float *); };
-        if (ks <= 36) hipLaunchKernelGGL((k_decode_wide_sb<36, 8>), grid, dim3(64 * kWideWaves), lds_for(36), s, w);
+        if (ks <= 36) hipLaunchKernelGGL((k_decode_split<8>), grid, dim3(64 * kSplitWaves), kSplitDecLds, s, w);
         else if (ks <= 40) hipLaunchKernelGGL((k_decode_wide<40, 8>), grid, dim3(kThreads), lds_for(40), s, w);
         else if (ks <= 44) hipLaunchKernelGGL((k_decode_wide<44, 8>), grid, dim3(kThreads), lds_for(44), s, w);
         else hipLaunchKernelGGL((k_decode_wide<48, 8>), grid, dim3(kThreads), lds_for(48), s, w);

@@ -148,3 +148,16 @@ def test_committed_profiles_are_consistent():
         assert 0.97 <= ratio <= 1.03, (fam, ratio)
     for f in os.listdir(os.path.join(ROOT, "profiles")):
         assert f.endswith((".txt", ".md")), f
+
+
+def test_contraction_peak_names_the_split_kernels():
+    """The c = 128 interior encode, and the decode with K <= 144, run six bf16
+    MFMA products per fp32 product: their fp32-equivalent roof is the bf16
+    peak over six, which puts their 32 flop per byte below the ridge (HBM
+    bound); the other stages keep the fp32 MFMA peak."""
+    peak, how = bench.contraction_peak("encode", 128, 143)
+    assert abs(peak - 2500.0 / 6) < 1e-9 and "bf16" in how
+    assert bench.contraction_peak("decode", 128, 144)[0] == peak
+    assert bench.contraction_peak("decode", 128, 145)[0] == bench.FP32_MFMA_PEAK_TFLOPS
+    assert bench.contraction_peak("encode", 64, 71)[0] == bench.FP32_MFMA_PEAK_TFLOPS
+    assert 32 < peak * 1e12 / (bench.HBM_PEAK_GBS * 1e9)

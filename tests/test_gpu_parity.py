@@ -49,10 +49,13 @@ def test_encode_with_permutations_is_exact(N, c, d):
 
 
 @pytest.mark.parametrize("N,c,d,misalign", [(4, 4, 4096, 0), (3, 7, 1001, 0), (8, 64, 64 * 500 + 7, 0),
-                                            (8, 16, 16 * 1024, 1), (2, 128, 128 * 70, 0), (5, 9, 9 * 64, 0)])
+                                            (8, 16, 16 * 1024, 1), (2, 128, 128 * 70, 0), (5, 9, 9 * 64, 0),
+                                            (2, 128, 128 * 640 - 17, 0)])
 def test_encode_matches_oracle_within_dot_product_bound(N, c, d, misalign):
     """|delta_gpu - delta| <= (c + 4) u32 (|G| |U|) elementwise: fp32-rounded
-    coefficients, fp32 products and any summation order fit this bound."""
+    coefficients, fp32 products and any summation order fit this bound, and
+    so do the c = 128 interior blocks, whose products are split into three
+    bf16 terms each (the last case: interior blocks and a ragged tail)."""
     U, R = orthogonal_plan(N, c, seed=N + c)
     U = U * np.random.default_rng(1).uniform(0.5, 2.0, size=(N, 1, c))   # not orthogonal any more
     plan = C.Plan.explicit(U, R)
@@ -68,6 +71,35 @@ def test_encode_matches_oracle_within_dot_product_bound(N, c, d, misalign):
         bound = (c + 4) * U32 * (np.abs(G) @ np.abs(U[i])) + 1e-38
         got = work[i, :c * p].double().cpu().numpy().reshape(c, p).T
         assert np.all(np.abs(got - exact) <= bound)
+
+
+@pytest.mark.parametrize("N,c,d", [(4, 16, 16 * 1024), (3, 64, 64 * 500 + 7), (4, 128, 128 * 640 - 17),
+                                   (2, 128, 128 * 70), (18, 128, 128 * 128)])
+def test_decode_matches_oracle_within_dot_product_bound(N, c, d):
+    """The decode applied to the device's own observations after round L,
+    against the oracle's decode of those observations (Sec. II-A):
+    |err| <= (K + 4) u32 (|Y| |R|), K = L + 1.  Covers the c = 128 interior
+    kernel on split bf16 operands (K <= 144), its ragged tail, the generic
+    kernel alone, and c = 128 with K = 145 (the fp32 wide kernel)."""
+    U, R = orthogonal_plan(N, c, seed=N + c + 1)
+    R = R * np.random.default_rng(2).uniform(0.5, 2.0, size=(N, R.shape[1], 1))
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=4)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    for k in range(plan.L + 1):
+        C.encode_round(plan, k, d, grads, work, ws)
+    C.decode(plan, d, work, ws, out)
+    sync()
+    sm = plan.slot_map(plan.L)
+    K = plan.L + 1
+    got_all = out.double().cpu().numpy()
+    for i in range(N):
+        cols = [sm[i, c + j] for j in range(N - 1)] + [sm[i, j] for j in range(c)]   # [B_1..B_{N-1} | D_1..D_c]
+        Y = np.column_stack([read_slot(plan, d, work, ws, s) for s in cols])
+        exact = OR.decode(Y, R[i]).T.reshape(-1)[:d]
+        bound = ((K + 4) * U32 * (np.abs(Y) @ np.abs(R[i]))).T.reshape(-1)[:d] + 1e-38
+        assert np.all(np.abs(got_all[i] - exact) <= bound), i
 
 
 # --- K2/K3 rounds: per-round buffer state ---------------------------------------------
