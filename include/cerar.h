@@ -335,11 +335,13 @@ int cerar_copy_f32(float *dst, const float *src, size_t n, cerar_stream stream);
 /* Measurement and test input (not part of the method): the seeded
  * synthetic gradient entries of the benchmark workloads, generated on the
  * device.  out[t] (device, n floats) = entry first + t of the stream `key`:
- * the Irwin-Hall sum of twelve 32-bit halves of splitmix64 hashes of
- * key + (8 idx + slot + 1) * 0x9E3779B97F4A7C15 (slots 0..5) minus 6, times
- * outlier_factor when the low half of slot 6 is below outlier_threshold (0:
- * never), times the scale of the tensor that holds idx (one fp64 product),
- * rounded once to fp32; 0 for idx >= d (the zero pad).  Tensor j covers flat
+ * with h_s the splitmix64 hash of key + (8 idx + s + 1) * 0x9E3779B97F4A7C15,
+ * the Box-Muller normal z = sqrt(-2 ln u1) cos(2 pi u2) of u1 = ((h_0 >> 11)
+ * + 1) 2^-53 and u2 = (h_1 >> 11) 2^-53 (the logarithm and cosine as fixed
+ * sequences of IEEE double operations, |z| <= 8.57), times outlier_factor
+ * when the low half of h_6 is below outlier_threshold (0: never), times the
+ * scale of the tensor that holds idx (one fp64 product), rounded once to
+ * fp32; 0 for idx >= d (the zero pad).  Tensor j covers flat
  * indices [tensor_off[j], tensor_off[j+1]); tensor_off (int64, ntensors + 1
  * entries, ascending, tensor_off[0] = 0) and tensor_scale (fp32, ntensors)
  * are device arrays owned by the caller.  The host generator of the tests

@@ -8,9 +8,14 @@
 //    Flood, "Fast splittable pseudorandom number generators", OOPSLA 2014,
 //    with its published constants) applied to key + counter * golden gamma,
 //    counter = 8 * index + slot + 1;
-//  * an approximately standard normal value, the Irwin-Hall sum of the twelve
-//    32-bit halves of slots 0..5 minus 6, in exact integer arithmetic and one
-//    exact scaling by 2^-32;
+//  * a standard normal value by the Box-Muller transform (Box & Muller, Ann.
+//    Math. Statist. 1958), z = sqrt(-2 ln u1) cos(2 pi u2), with u1 in (0, 1]
+//    from the top 53 bits of slot 0 and u2 in [0, 1) from those of slot 1.
+//    The logarithm (an exact binary split, then an atanh series) and the
+//    cosine (an exact octant reduction, then Taylor series on [0, pi/4]) are
+//    IEEE double additions, multiplications and divisions in a fixed order,
+//    with fused multiply-adds off, and the square root is correctly rounded,
+//    so the host generator's steps give the same bits;
 //  * an outlier when the low half of slot 6 is below a threshold, which
 //    multiplies the value by a factor (fp64);
 //  * the entry is float32(value * scale of its tensor): one fp64 product,
@@ -42,6 +47,54 @@ __device__ inline uint64_t slot_bits(uint64_t key, uint64_t idx, int slot) {
     return mix64(key + (idx * 8 + (uint64_t)(slot + 1)) * kGolden);
 }
 
+constexpr double kLn2 = 0.693147180559945309417;
+constexpr double kSqrtHalf = 0.707106781186547524401;
+constexpr double kPi4 = 0.785398163397448309616;
+constexpr int kAtanhTerms = 11;
+
+// (-1)^k / n!, n = first + 2k, with n! an exact double product (n <= 18).
+constexpr double taylor_coefficient(int first, int k) {
+    double f = 1.0;
+    for (int i = 2; i <= first + 2 * k; ++i) f = f * (double)i;
+    return (k % 2 ? -1.0 : 1.0) / f;
+}
+
+// ln u for u in (0, 1]: u = m 2^e exactly, m in [sqrt(1/2), sqrt(2)), and
+// ln m = 2 atanh(t), t = (m - 1) / (m + 1).
+__device__ inline double ln_unit(double u) {
+#pragma clang fp contract(off)
+    int e;
+    double m = frexp(u, &e);
+    if (m < kSqrtHalf) {
+        m = m * 2.0;
+        e = e - 1;
+    }
+    const double t = (m - 1.0) / (m + 1.0);
+    const double t2 = t * t;
+    double acc = 1.0 / (double)(2 * kAtanhTerms - 1);
+#pragma unroll
+    for (int k = kAtanhTerms - 2; k >= 0; --k) acc = acc * t2 + 1.0 / (double)(2 * k + 1);
+    return (double)e * kLn2 + 2.0 * (t * acc);
+}
+
+// cos(2 pi u) from w8 = 8 u (exact) and its octant o: phi = (f or 1 - f) pi/4.
+__device__ inline double cos_2pi(double w8, int o) {
+#pragma clang fp contract(off)
+    const double f = w8 - (double)o;
+    const double a = (o & 1) ? 1.0 - f : f;
+    const double phi = a * kPi4;
+    const double p2 = phi * phi;
+    double c = taylor_coefficient(0, 9);
+#pragma unroll
+    for (int k = 8; k >= 0; --k) c = c * p2 + taylor_coefficient(0, k);
+    double sn = taylor_coefficient(1, 8);
+#pragma unroll
+    for (int k = 7; k >= 0; --k) sn = sn * p2 + taylor_coefficient(1, k);
+    sn = sn * phi;
+    const double v = (o == 1 || o == 2 || o == 5 || o == 6) ? sn : c;
+    return (o >= 2 && o <= 5) ? -v : v;
+}
+
 struct SynthArgs {
     float *out;
     uint64_t n, first, d, key;
@@ -54,14 +107,12 @@ struct SynthArgs {
 
 __device__ inline float entry(const SynthArgs &a, uint64_t idx, const int64_t *soff, const float *sscale,
                               int &t) {
+#pragma clang fp contract(off)
     if (idx >= a.d) return 0.0f;                          // the zero pad
-    int64_t total = 0;
-#pragma unroll
-    for (int j = 0; j < 6; ++j) {
-        const uint64_t h = slot_bits(a.key, idx, j);
-        total += (int64_t)(h & 0xFFFFFFFFull) + (int64_t)(h >> 32);
-    }
-    double v = (double)(total + 6 - 6 * ((int64_t)1 << 32)) * 0x1.0p-32;
+    const double u1 = (double)((slot_bits(a.key, idx, 0) >> 11) + 1) * 0x1.0p-53;
+    const uint64_t i2 = slot_bits(a.key, idx, 1) >> 11;
+    const double w8 = (double)i2 * 0x1.0p-50;
+    double v = sqrt(-2.0 * ln_unit(u1)) * cos_2pi(w8, (int)(i2 >> 50));
     if (a.threshold != 0 && (uint32_t)(slot_bits(a.key, idx, 6) & 0xFFFFFFFFull) < a.threshold) v = v * a.factor;
     while (t + 1 < a.ntensors && (uint64_t)soff[t + 1] <= idx) ++t;   // the tensor that holds idx
     return (float)(v * (double)sscale[t]);

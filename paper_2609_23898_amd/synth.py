@@ -9,11 +9,19 @@ makes numbers.  Every value is a pure function of (seed, stream, index):
 * a counter-based splitmix64 hash (Steele, Lea & Flood, "Fast splittable
   pseudorandom number generators", OOPSLA 2014; the 64-bit finaliser constants
   as published with splitmix64) gives 64 random bits per counter;
-* an approximately standard normal value is the Irwin-Hall sum of twelve
-  32-bit uniforms minus 6.  It is computed with exact integer arithmetic and
-  one exact scaling by 2^-32, so this NumPy path and the library's device
-  generator (cerar_synth_fill, which the device-side callers use) produce
-  the same bits;
+* a gradient entry's standard normal value comes from the Box-Muller
+  transform (Box & Muller, "A note on the generation of random normal
+  deviates", Ann. Math. Statist. 1958), z = sqrt(-2 ln u1) cos(2 pi u2), of
+  two 53-bit uniforms.  The logarithm (an atanh series after an exact
+  binary split) and the cosine (an octant reduction that is exact and Taylor
+  series on [0, pi/4]) are written out here in IEEE double additions,
+  multiplications and divisions in a fixed order, and the square root is
+  the correctly rounded one, so the library's device generator
+  (cerar_synth_fill, which computes the same steps without fused
+  multiply-adds) produces the same bits.  The tails reach |z| = 8.57;
+* the plan-side numbers (the random base matrix, the per-tensor log-normal
+  scales) use an Irwin-Hall sum of twelve 32-bit uniforms minus 6 instead,
+  computed exactly in integers: approximately normal, bounded at 6;
 * a gradient entry is float32(normal * scale), where the scale comes from a
   per-tensor table computed once on the host.  Every path does the same
   single float64 product and the same single rounding to float32.
@@ -81,6 +89,83 @@ def normal_np(key, idx):
             total += (h & np.uint64(0xFFFFFFFF)).astype(np.int64)
             total += (h >> np.uint64(32)).astype(np.int64)
     return (total + 6 - 6 * (1 << 32)).astype(np.float64) * 2.0 ** -32
+
+
+# Box-Muller in IEEE double operations in a fixed order (no fused
+# multiply-add, no library transcendental), mirrored step for step by the
+# device generator.
+_LN2 = 0.693147180559945309417
+_SQRT_HALF = 0.707106781186547524401
+_PI_4 = 0.785398163397448309616
+
+
+def _taylor_coefficients(first, count):
+    """(-1)^k / n! for n = first + 2k: n! as an exact double product
+    (n <= 18, below the 2^53 limit), then one division."""
+    out = []
+    for k in range(count):
+        n = first + 2 * k
+        f = 1.0
+        for i in range(2, n + 1):
+            f = f * float(i)
+        out.append((-1.0 if k % 2 else 1.0) / f)
+    return out
+
+
+_COS_C = _taylor_coefficients(0, 10)     # 1/0!, -1/2!, ..., 1/18!
+_SIN_C = _taylor_coefficients(1, 9)      # 1/1!, -1/3!, ..., 1/17!
+_ATANH_N = 11                        # odd terms t^(2k+1)/(2k+1), k < 11
+
+
+def _ln_unit_np(u):
+    """ln u for u in (0, 1]: u = m 2^e exactly with m in [sqrt(1/2), sqrt(2)),
+    ln m = 2 atanh(t), t = (m - 1) / (m + 1), |t| <= 0.172."""
+    m, e = np.frexp(u)
+    low = m < _SQRT_HALF
+    m = np.where(low, m * 2.0, m)
+    e = np.where(low, e - 1, e).astype(np.float64)
+    t = (m - 1.0) / (m + 1.0)
+    t2 = t * t
+    acc = np.full(u.shape, 1.0 / float(2 * _ATANH_N - 1))
+    for k in range(_ATANH_N - 2, -1, -1):
+        acc = acc * t2 + 1.0 / float(2 * k + 1)
+    return e * _LN2 + 2.0 * (t * acc)
+
+
+def _cos_2pi_np(w8, o):
+    """cos(2 pi u) from w8 = 8u (exact) and its octant o = floor(w8): with
+    f = w8 - o, phi = (f or 1 - f) pi/4 in [0, pi/4] and a sign."""
+    f = w8 - o
+    odd = (o % 2) == 1
+    a = np.where(odd, 1.0 - f, f)
+    phi = a * _PI_4
+    p2 = phi * phi
+    c = np.full(phi.shape, _COS_C[-1])
+    for k in range(len(_COS_C) - 2, -1, -1):
+        c = c * p2 + _COS_C[k]
+    s = np.full(phi.shape, _SIN_C[-1])
+    for k in range(len(_SIN_C) - 2, -1, -1):
+        s = s * p2 + _SIN_C[k]
+    s = s * phi
+    use_sin = np.isin(o, (1, 2, 5, 6))
+    neg = np.isin(o, (2, 3, 4, 5))
+    v = np.where(use_sin, s, c)
+    return np.where(neg, -v, v)
+
+
+def gauss_np(key, idx):
+    """Box-Muller standard normal at the given counters, float64: u1 from
+    hash slot 0 in (0, 1], u2 from slot 1 in [0, 1), 53 bits each."""
+    idx = np.asarray(idx, dtype=np.int64)
+    with np.errstate(over="ignore"):
+        h1 = _hash_np(key, idx, 0)
+        h2 = _hash_np(key, idx, 1)
+    u1 = ((h1 >> np.uint64(11)) + np.uint64(1)).astype(np.float64) * 2.0 ** -53
+    i2 = (h2 >> np.uint64(11)).astype(np.int64)
+    o = (i2 >> 50).astype(np.int64)                    # floor(8 u2)
+    w8 = i2.astype(np.float64) * 2.0 ** -50            # 8 u2, exact
+    r = np.sqrt(-2.0 * _ln_unit_np(u1))
+    return r * _cos_2pi_np(w8, o)
 
 
 def uniform32_np(key, idx, j):
@@ -195,7 +280,7 @@ class Workload:
         valid = flat_idx < self.d
         idx = np.where(valid, flat_idx, 0)
         key = self.worker_key(worker)
-        n = normal_np(key, idx)
+        n = gauss_np(key, idx)
         if self.outlier_prob > 0:
             hit = uniform32_np(key, idx, 6) < self.outlier_threshold
             n = np.where(hit, n * float(self.outlier_factor), n)

@@ -1,7 +1,7 @@
 /* A C consumer of libcerar: one approximate all-reduce of N workers'
  * gradients on the current GPU through the C ABI and the HIP runtime alone,
  * with no Python.  The inputs come from the library's seeded generator
- * (cerar_synth_fill, Irwin-Hall normals in [-6, 6]).  Two plans:
+ * (cerar_synth_fill, Box-Muller normals, |z| <= 8.6).  Two plans:
  *  - exact (c = N, eps = 0, Sec. II-B): every output must be the sum of the
  *    N gradients up to fp32 rounding of the coefficients (1e-5 relative);
  *  - condition-number constrained (c > N, kappa_max = 1e3, Sec. II-D): an
@@ -75,7 +75,7 @@ static int run(int N, int c, cerar_construction kind, double param, size_t d, do
         for (int w = 0; w < N; ++w) sum[e] += hg[(size_t)w * d + e];
     }
     int finite_inputs = 1;
-    for (size_t i = 0; i < (size_t)N * d; ++i) finite_inputs &= isfinite(hg[i]) && fabsf(hg[i]) <= 6.0f;
+    for (size_t i = 0; i < (size_t)N * d; ++i) finite_inputs &= isfinite(hg[i]) && fabsf(hg[i]) <= 8.6f;
     if (!finite_inputs || sum[0] == 0.0) {
         fprintf(stderr, "generated inputs out of range\n");
         return 1;

@@ -34,8 +34,42 @@ def _value_python(wl, worker, idx):
     def bits(slot):
         return synth._mix64_int((key + (idx * 8 + slot + 1) * synth._GOLDEN) & synth._MASK64)
 
-    total = sum((h & 0xFFFFFFFF) + (h >> 32) for h in (bits(j) for j in range(6)))
-    v = float(total + 6 - 6 * (1 << 32)) * 2.0 ** -32
+    # Box-Muller: u1 in (0, 1] and u2 in [0, 1) from the top 53 bits of slots 0 and 1
+    u1 = float((bits(0) >> 11) + 1) * 2.0 ** -53
+    i2 = bits(1) >> 11
+    # ln u1 = e ln 2 + 2 atanh(t), u1 = m 2^e, m in [sqrt(1/2), sqrt(2)), t = (m - 1)/(m + 1)
+    m, e = math.frexp(u1)
+    if m < 0.707106781186547524401:
+        m, e = m * 2.0, e - 1
+    t = (m - 1.0) / (m + 1.0)
+    acc = 1.0 / 21.0
+    for k in range(9, -1, -1):
+        acc = acc * (t * t) + 1.0 / float(2 * k + 1)
+    ln_u1 = float(e) * 0.693147180559945309417 + 2.0 * (t * acc)
+    # cos(2 pi u2) by octants: 2 pi u2 = (pi/4)(o + f)
+    w8 = float(i2) * 2.0 ** -50
+    o = i2 >> 50
+    f = w8 - float(o)
+    phi = (1.0 - f if o % 2 else f) * 0.785398163397448309616
+    p2 = phi * phi
+
+    def coef(first, k):
+        fact = 1.0
+        for i in range(2, first + 2 * k + 1):
+            fact = fact * float(i)
+        return (-1.0 if k % 2 else 1.0) / fact
+
+    c = coef(0, 9)
+    for k in range(8, -1, -1):
+        c = c * p2 + coef(0, k)
+    sn = coef(1, 8)
+    for k in range(7, -1, -1):
+        sn = sn * p2 + coef(1, k)
+    sn = sn * phi
+    cv = sn if o in (1, 2, 5, 6) else c
+    if o in (2, 3, 4, 5):
+        cv = -cv
+    v = math.sqrt(-2.0 * ln_u1) * cv
     if wl.outlier_prob > 0 and (bits(6) & 0xFFFFFFFF) < wl.outlier_threshold:
         v = v * float(wl.outlier_factor)
     t = bisect.bisect_right(list(wl._offsets), idx) - 1
@@ -61,8 +95,29 @@ def test_numpy_path_matches_the_definition():
     assert np.abs(wl.values_np(1, np.arange(20000))).max() > 6      # outliers are in the check
 
 
+def test_box_muller_normal_is_standard_normal():
+    """The gradient entries' normal: moments, a Kolmogorov-Smirnov test and
+    the tail beyond 4 sigma of N(0, 1), and its logarithm and cosine against
+    the library functions to within a few units of double rounding."""
+    from scipy import stats
+    z = synth.gauss_np(synth.stream_key(1, 1), np.arange(2_000_000))
+    assert abs(z.mean()) < 3e-3 and abs(z.var() - 1.0) < 3e-3
+    assert abs(np.mean(z ** 4) - 3.0) < 0.03
+    assert stats.kstest(z, "norm").pvalue > 0.01
+    tail = np.mean(np.abs(z) > 4.0)                      # 6.33e-5 for N(0, 1)
+    assert 3.5e-5 < tail < 9.5e-5 and np.abs(z).max() > 4.5
+    rng = np.random.default_rng(7)
+    u = (rng.integers(0, 1 << 53, 200_000) + 1).astype(np.float64) * 2.0 ** -53
+    ln = synth._ln_unit_np(u)
+    assert np.max(np.abs(ln - np.log(u)) / np.maximum(np.abs(np.log(u)), 1e-300)) < 4e-15
+    i2 = rng.integers(0, 1 << 53, 200_000)
+    w8 = i2.astype(np.float64) * 2.0 ** -50
+    cos = synth._cos_2pi_np(w8, (i2 >> 50).astype(np.int64))
+    assert np.max(np.abs(cos - np.cos(2.0 * np.pi * (i2.astype(np.float64) * 2.0 ** -53)))) < 4e-15
+
+
 def test_irwin_hall_normal_moments():
-    # Irwin-Hall(12) - 6 has mean 0, variance exactly 1, support [-6, 6]
+    # Irwin-Hall(12) - 6 (plan-side numbers) has mean 0, variance exactly 1, support [-6, 6]
     x = synth.normal_np(synth.stream_key(1, 1), np.arange(1_000_000))
     assert abs(x.mean()) < 5e-3
     assert abs(x.var() - 1.0) < 5e-3
@@ -87,7 +142,7 @@ def test_outliers_are_one_percent_at_100x():
     hit = synth.uniform32_np(key, idx, 6) < wl.outlier_threshold
     assert abs(hit.mean() - 0.01) < 1e-3
     v = wl.values_np(3, idx).astype(np.float64)
-    base = synth.normal_np(key, idx)
+    base = synth.gauss_np(key, idx)
     np.testing.assert_allclose(v[hit], (base[hit] * 100.0).astype(np.float32), rtol=0)
     np.testing.assert_allclose(v[~hit], base[~hit].astype(np.float32), rtol=0)
 
@@ -111,7 +166,7 @@ def test_per_tensor_scales_are_lognormal_and_shared():
     t = 5
     idx = np.arange(off[t], off[t] + 1000)
     for w in (0, 7):
-        ratio = wl.values_np(w, idx).astype(np.float64) / synth.normal_np(wl.worker_key(w), idx)
+        ratio = wl.values_np(w, idx).astype(np.float64) / synth.gauss_np(wl.worker_key(w), idx)
         np.testing.assert_allclose(ratio, s[t], rtol=1e-6)
 
 
