@@ -62,6 +62,8 @@ def parse():
                     help="write the summary of a rocprofv3 --kernel-trace --stats run of this bench")
     ap.add_argument("--traced-args", default="",
                     help="with --summarize-trace: the flags the traced bench.py run was given")
+    ap.add_argument("--pmc-workload", default=None,
+                    help="with --summarize-pmc: the workload the counter runs were taken on (default: the headline)")
     ap.add_argument("--summarize-pmc", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"),
                     help="write the HBM traffic summary of two rocprofv3 --pmc runs of this bench")
     return ap.parse_args()
@@ -71,6 +73,9 @@ def parse():
 
 KERNEL_SOURCES = ("paper_2609_23898_amd/csrc/kernels.hip", "paper_2609_23898_amd/csrc/cerar_internal.hpp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_cerar_n8_c64_pythia1.4b.txt")
+# committed counter summaries per workload (the headline's is TRAFFIC_FILE)
+TRAFFIC_FILES = {"pythia-1.4b": TRAFFIC_FILE,
+                 "heavytail-n16-c128": os.path.join(ROOT, "profiles", "hbm_traffic_cerar_n16_c128_heavytail.txt")}
 FAMILIES = (("k_encode", "k_encode (K1)"), ("k_round<0,", "k_round<0> (K2: recv + delta)"),
             ("k_round<1,", "k_round<1> (K3: recv - delta + delta)"),
             ("k_round<2,", "k_round<2> (K3: recv - delta)"), ("k_decode", "k_decode (K4)"),
@@ -118,13 +123,15 @@ def _read_csv(path):
         return list(csv.DictReader(f))
 
 
-def _step_bytes_cfg4():
-    """Algorithmic bytes per launch of each family at the Pythia-1.4B workload."""
+def _launch_bytes(workload=None):
+    """Algorithmic bytes per launch of each family at a workload (default: the
+    Pythia-1.4B headline), with the library's chunk length: ceil(d / c)
+    rounded up to a multiple of 32 floats."""
     from paper_2609_23898_amd import cerar as C
     from paper_2609_23898_amd import synth
-    wl = synth.workload("pythia-1.4b")
+    wl = synth.workload(workload or synth.HEADLINE)
     N, c = wl.N, wl.c
-    p = -(-wl.d // c)                            # a multiple of 32 here: the library's p too
+    p = -(-(-(-wl.d // c)) // 32) * 32
     bw = C.phase_bytes_per_worker(N, c, p)
     return {"k_encode (K1)": N * bw["encode"], "k_decode (K4)": N * bw["decode"],
             "k_round<0> (K2: recv + delta)": N * bw["rounds"][1],
@@ -216,22 +223,26 @@ def _pmc_per_family(d, counter, copy_grid=None):
     return {fam: (v / n, n) for fam, (v, n) in acc.items()}
 
 
-def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30):
+def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30, workload=None):
+    from paper_2609_23898_amd import synth
     fetch = _pmc_per_family(fetch_dir, "FETCH_SIZE", copy_grid=copy_floats // 4)
     write = _pmc_per_family(write_dir, "WRITE_SIZE", copy_grid=copy_floats // 4)
     copy = "k_copy4 (copy reference)"
     copy_kib = copy_floats * 4 / 1024.0
     f_scale = fetch[copy][0] / copy_kib
     w_scale = write[copy][0] / copy_kib
-    algo = _step_bytes_cfg4()
+    algo = _launch_bytes(workload)
+    wl = synth.workload(workload or synth.HEADLINE)
+    wflag = f" --workload {workload}" if workload else ""
     lines = ["# HBM traffic per dispatch from rocprofv3 counters (FETCH_SIZE, WRITE_SIZE in KiB per dispatch)",
-             "# workload: N=8 workers, c=64, d=1,414,647,808 fp32 (Pythia-1.4B-shaped), kappa_max=1e3 plan",
+             f"# workload: {wl.name} (N={wl.N}, c={wl.c}, d={wl.d}, fp32)",
              "# commands (repo root, MI355X), one counter per run:",
              "#   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
-             f"-d {fetch_dir} -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
+             f"-d {fetch_dir} -o pmc -- python3 bench.py{wflag} --steps 1 --warmup 0 --cpu-positions 0",
              "#   rocprofv3 --pmc WRITE_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
-             f"-d {write_dir} -o pmc -- python3 bench.py --steps 1 --warmup 0 --cpu-positions 0",
-             f"#   python3 bench.py --summarize-pmc {fetch_dir} {write_dir} {out_path}",
+             f"-d {write_dir} -o pmc -- python3 bench.py{wflag} --steps 1 --warmup 0 --cpu-positions 0",
+             f"#   python3 bench.py --summarize-pmc {fetch_dir} {write_dir} {out_path}"
+             + (f" --pmc-workload {workload}" if workload else ""),
              "# scale: each counter divided by what it reads for the plain copy kernel k_copy4 moving "
              f"{copy_floats} floats ({copy_kib:.0f} KiB read and written per dispatch)",
              f"kernel_source_sha256: {kernel_source_hash()}",
@@ -252,11 +263,15 @@ def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30):
     print("\n".join(lines))
 
 
-def committed_traffic(family):
-    """HBM bytes per launch of `family` from the committed counter summary, or
-    None when there is none or the kernels changed since it was taken."""
+def committed_traffic(family, workload=None):
+    """HBM bytes per launch of `family` from the workload's committed counter
+    summary, or None when there is none or the kernels changed since it was
+    taken."""
+    path = TRAFFIC_FILES.get(workload or "pythia-1.4b")
+    if path is None:
+        return None
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             text = f.read()
     except OSError:
         return None
@@ -452,7 +467,7 @@ def main():
         summarize_trace(*args.summarize_trace, bench_args=args.traced_args.split())
         return
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, copy_floats=args.copy_floats)
+        summarize_pmc(*args.summarize_pmc, copy_floats=args.copy_floats, workload=args.pmc_workload)
         return
     if args.gpus != 1:
         print(f"bench.py runs the single-GPU simulation of all N workers; --gpus {args.gpus} is not "
@@ -627,8 +642,8 @@ def main():
     else:
         roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(dk["gbps"], 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dk["gbps"] / HBM_PEAK_GBS, 4),
-                    # the committed counter summary covers the headline workload only
-                    "traffic": committed_traffic(dominant) if args.workload == synth.HEADLINE else None}
+                    # from the workload's committed counter summary, where there is one
+                    "traffic": committed_traffic(dominant, args.workload)}
 
     # achievable-bandwidth reference: a plain copy kernel
     nf = min(args.copy_floats, grads.numel())

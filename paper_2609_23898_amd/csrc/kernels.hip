@@ -249,11 +249,10 @@ __device__ inline void mtile2_mma_lds2(v4f (&acc)[2][2], const v2f (&b)[KS], con
 
 // Copies nmt M-tiles of fragments [mt][ks][lane] (KSx K-steps) into LDS as
 // [mt][q][lane][r], ks = 4q + r, zero-padded to KSpad K-steps.
-__device__ inline void stage_fragments_padded(float *sfrag, const float *gfrag, int nmt, int KSx, int KSpad,
-                                              int nthreads = kThreads) {
+__device__ inline void stage_fragments_padded(float *sfrag, const float *gfrag, int nmt, int KSx, int KSpad) {
     const int Q = (KSpad + 3) / 4;
     const int total = nmt * Q * 256;
-    for (int idx = threadIdx.x; idx < total; idx += nthreads) {
+    for (int idx = threadIdx.x; idx < total; idx += kThreads) {
         const int r = idx & 3, ln = (idx >> 2) & 63, q = (idx >> 8) % Q, mt = (idx >> 8) / Q;
         const int ks = q * 4 + r;
         sfrag[idx] = ks < KSx ? gfrag[((size_t)mt * KSx + ks) * 64 + ln] : 0.f;

@@ -7,6 +7,7 @@ import os
 import subprocess
 import sys
 
+import numpy as np
 import pytest
 
 import bench
@@ -44,7 +45,7 @@ def test_headline_step_bytes_and_launch_families():
     assert fams.count("k_round<1> (K3: recv - delta + delta)") == c - N == 56
     assert fams.count("k_round<2> (K3: recv - delta)") == N - 2 == 6
     assert fams[-1] is None
-    per_launch = bench._step_bytes_cfg4()
+    per_launch = bench._launch_bytes()
     assert per_launch["k_round<1> (K3: recv - delta + delta)"] == N * 4 * p * 4
     assert per_launch["k_encode (K1)"] == N * (2 * c + 1) * p * 4
 
@@ -54,6 +55,8 @@ def test_kernel_names_map_to_families():
     assert bench.family_of_name("k_round<1, true>") == "k_round<1> (K3: recv - delta + delta)"
     assert bench.family_of_name("k_round<0, false>") == "k_round<0> (K2: recv + delta)"
     assert bench.family_of_name("k_decode_wide<48, 8>") == "k_decode (K4)"
+    assert bench.family_of_name("k_encode_split<8>") == "k_encode (K1)"
+    assert bench.family_of_name("k_decode_split<8>") == "k_decode (K4)"
     assert bench.family_of_name("k_copy4") == "k_copy4 (copy reference)"
     assert bench.family_of_name("k_fused_lanes<4, 8, true>") is None
     assert bench.family_of_name("k_norms") is None
@@ -135,7 +138,7 @@ def test_committed_profiles_are_consistent():
     bench's HIP events within 3 % for the launches that dominate the step."""
     import re as _re
     text = open(bench.TRAFFIC_FILE).read()
-    algo = bench._step_bytes_cfg4()
+    algo = bench._launch_bytes()
     for fam, a in algo.items():
         m = _re.search(r"^traffic_bytes_per_launch\[" + _re.escape(fam) + r"\]: (\d+)", text, _re.M)
         assert m, fam
@@ -148,6 +151,15 @@ def test_committed_profiles_are_consistent():
         assert 0.97 <= ratio <= 1.03, (fam, ratio)
     for f in os.listdir(os.path.join(ROOT, "profiles")):
         assert f.endswith((".txt", ".md")), f
+    # the c = 128 counter summary: the split-operand encode and decode and the
+    # rounds move their algorithmic bytes
+    path = bench.TRAFFIC_FILES["heavytail-n16-c128"]
+    if os.path.exists(path):
+        text = open(path).read()
+        for fam, a in bench._launch_bytes("heavytail-n16-c128").items():
+            m = _re.search(r"^traffic_bytes_per_launch\[" + _re.escape(fam) + r"\]: (\d+)", text, _re.M)
+            assert m, fam
+            assert 0.98 <= int(m.group(1)) / a <= 1.06, (fam, int(m.group(1)) / a)
 
 
 def test_contraction_peak_names_the_split_kernels():
@@ -161,3 +173,17 @@ def test_contraction_peak_names_the_split_kernels():
     assert bench.contraction_peak("decode", 128, 145)[0] == bench.FP32_MFMA_PEAK_TFLOPS
     assert bench.contraction_peak("encode", 64, 71)[0] == bench.FP32_MFMA_PEAK_TFLOPS
     assert 32 < peak * 1e12 / (bench.HBM_PEAK_GBS * 1e9)
+
+
+def test_launch_bytes_use_the_library_chunk_length():
+    """Per-launch algorithmic bytes of a workload whose d is not a multiple
+    of 32 c: the chunk length is the library's (ceil(d / c) rounded up to 32)."""
+    from paper_2609_23898_amd import synth
+    wl = synth.workload("heavytail-n16-c128")
+    plan = C.Plan.explicit(np.stack([np.eye(wl.c)] * wl.N), np.zeros((wl.N, wl.c + wl.N - 1, wl.c)))
+    p, _ = plan.chunk_len(wl.d)
+    assert p % 32 == 0 and p * wl.c >= wl.d and p != wl.d // wl.c
+    b = bench._launch_bytes("heavytail-n16-c128")
+    assert b["k_encode (K1)"] == wl.N * (2 * wl.c + 1) * p * 4
+    assert b["k_decode (K4)"] == wl.N * (2 * wl.c + wl.N - 1) * p * 4
+    assert b["k_round<1> (K3: recv - delta + delta)"] == wl.N * 4 * p * 4
