@@ -205,22 +205,30 @@ def summarize_trace(trace_dir, bench_log, out_path, bench_args=()):
 
 
 def _pmc_per_family(d, counter, copy_grid=None):
-    """Mean counter value per dispatch of each family.  The copy kernel also
-    serves the bench's refills of other sizes: with copy_grid, only its
-    dispatches of that grid size (the reference copy) count."""
+    """Mean counter value per launch of each family, and the launch count.
+    An encode or decode launch can be two dispatches (the interior blocks'
+    kernel and the tail's), so a family's total is divided by its dispatches
+    over its distinct kernel names.  The copy kernel also serves the bench's
+    refills of other sizes: with copy_grid, only its dispatches of that grid
+    size (the reference copy) count."""
     rows = _read_csv(_find_csv(d, "counter_collection.csv"))
     acc = {}
     for r in rows:
         if r.get("Counter_Name") != counter:
             continue
-        fam = family_of_name(r["Kernel_Name"])
+        name = r["Kernel_Name"]
+        fam = None if "_batch" in name else family_of_name(name)
         if fam is None:
             continue
         if fam.startswith("k_copy4") and copy_grid is not None and int(r["Grid_Size"]) != copy_grid:
             continue
-        v, n = acc.get(fam, (0.0, 0))
-        acc[fam] = (v + float(r["Counter_Value"]), n + 1)
-    return {fam: (v / n, n) for fam, (v, n) in acc.items()}
+        v, n, names = acc.get(fam, (0.0, 0, set()))
+        acc[fam] = (v + float(r["Counter_Value"]), n + 1, names | {name})
+    out = {}
+    for fam, (v, n, names) in acc.items():
+        launches = n // len(names)
+        out[fam] = (v / launches, launches)
+    return out
 
 
 def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30, workload=None):
@@ -234,7 +242,8 @@ def summarize_pmc(fetch_dir, write_dir, out_path, copy_floats=1 << 30, workload=
     algo = _launch_bytes(workload)
     wl = synth.workload(workload or synth.HEADLINE)
     wflag = f" --workload {workload}" if workload else ""
-    lines = ["# HBM traffic per dispatch from rocprofv3 counters (FETCH_SIZE, WRITE_SIZE in KiB per dispatch)",
+    lines = ["# HBM traffic per launch from rocprofv3 counters (FETCH_SIZE, WRITE_SIZE in KiB; an encode or "
+             "decode launch is its interior and tail dispatches)",
              f"# workload: {wl.name} (N={wl.N}, c={wl.c}, d={wl.d}, fp32)",
              "# commands (repo root, MI355X), one counter per run:",
              "#   rocprofv3 --pmc FETCH_SIZE --kernel-include-regex 'k_(encode|round|decode|copy4)' -f csv "
