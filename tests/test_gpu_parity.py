@@ -200,6 +200,39 @@ def test_ring_simulate_parity(name, N, c, d, kind, param):
         assert err_orc < 1e-12 and err_gpu < 1e-5        # exact ring all-reduce (c = N)
 
 
+def _random_shapes(count, seed):
+    """Seeded (N, c, d) shapes: c = 128 with every decode kernel (K = c + N - 1
+    up to 144 on the split-operand kernel, above it on the fp32 one),
+    multiples of 16 and odd c, d with and without interior blocks."""
+    rng = np.random.default_rng(seed)
+    shapes = []
+    for t in range(count):
+        N = int(rng.integers(2, 19))
+        c = 128 if t % 3 == 0 else (16 * int(rng.integers(1, 9)) if t % 3 == 1 else int(rng.integers(N, 100)))
+        c = max(c, N)
+        p = 64 * int(rng.integers(1, 7)) + (int(rng.integers(0, 64)) if t % 2 else 0)
+        d = max(1, c * p - int(rng.integers(0, 3 * p if t % 4 == 3 else 64)))
+        shapes.append((N, c, d))
+    return shapes
+
+
+@pytest.mark.parametrize("N,c,d", _random_shapes(24, 2609))
+def test_random_shapes_match_oracle(N, c, d):
+    """The whole ring on a well-conditioned plan (orthogonal U_k, least-squares
+    R_i) over seeded random shapes, gated like the named cases."""
+    U, R = orthogonal_plan(N, c, seed=N * 7 + c)
+    kappa = OP.max_kappa_M(U)
+    plan = C.Plan.explicit(U, R)
+    g = host_grads(N, d, seed=d % 1000)
+    grads = to_device(g)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, grads, work, ws, out)
+    sync()
+    gpu = out.double().cpu().numpy()
+    assert np.all(np.isfinite(gpu))
+    assert max_rel_l2(gpu, oracle_allreduce(g, U, R)) <= gate(kappa), (N, c, d, kappa)
+
+
 EDGE = [
     # name, N, c, d: degenerate and extreme shapes
     ("d1", 4, 8, 1),                       # p = 1: seven chunks are pure padding
