@@ -711,7 +711,8 @@ def main():
     step_bytes = N * C.algorithmic_bytes_per_worker(N, c, p)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     result = {
-        "metric": METRIC,
+        "metric": METRIC if args.workload == synth.HEADLINE else
+                  f"encode+round+decode GB/s per worker (% HBM peak), N={N} c={c} d={d} fp32",
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
