@@ -56,9 +56,11 @@ def _check_replays(call, make_bufs, inputs, d, oracle_check):
     del graph
 
 
-def test_ring_simulate_replays_from_a_graph():
+@pytest.mark.parametrize("N,c,d", [(8, 32, 32 * 2048 + 7),     # pipelined encode and decode, ragged tail
+                                   (8, 64, 64 * 1024),         # double-buffered kernels
+                                   (4, 128, 128 * 640 - 5)])   # split-operand c = 128 kernels and the tail
+def test_ring_simulate_replays_from_a_graph(N, c, d):
     torch, dev = torch_dev()
-    N, c, d = 8, 32, 32 * 2048 + 7
     U, R = orthogonal_plan(N, c, seed=31)
     plan = C.Plan.explicit(U, R)
 
