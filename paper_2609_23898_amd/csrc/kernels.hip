@@ -2,12 +2,16 @@
 //
 //  k_encode  (K1)  delta_{i,j} = sum_l U_i[l][j] chunk_l(g_i), all workers,
 //                  as fp32 MFMA 16x16x4 tiles: delta^T = U^T G^T, positions
-//                  on the MFMA N axis, coefficients (A operand) from LDS.
+//                  on the MFMA N axis, coefficients (A operand) from LDS; at
+//                  c = 128 on bf16 MFMAs with fp32 operands split exactly
+//                  into three bf16 terms (k_encode_split).
 //  k_round   (K2/K3) one ring round for all workers: next message =
 //                  received (- returning own term) (+ next own term).
 //  k_decode  (K4)  g_hat_i = Y_i R_i, the same MFMA tiling over the L+1
-//                  stored observations, gathered through the slot table.
-//  k_norms   (K5)  per-worker squared error against S = sum_w g_w, fp64.
+//                  stored observations, gathered through the slot table
+//                  (k_decode_split at c = 128).
+//  k_norms   (K5)  per-worker squared error against S = sum_w g_w, fp64,
+//                  and on sampled positions against given reference values.
 //  k_copy          plain streaming copy (bandwidth reference).
 #include <hip/hip_runtime.h>
 
