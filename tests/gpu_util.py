@@ -104,3 +104,54 @@ def gate(kappa_M):
     if kappa_M <= 1e3:
         return 1e-4
     return max(1e-4, 64 * kappa_M * U32)
+
+
+def f32(x):
+    """Round to fp32 and back to fp64."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def fp32_observations(Delta, one_rounding=True):
+    """Y_i of Algorithm 1 with every message held in fp32 (the wire format):
+    x_{i,k+1} = recv + delta_{i,k+1} for k < N, recv - delta_{i,j}
+    (+ delta_{i,k+1}) for k >= N, rounded once per round (or once per
+    operation), all other arithmetic exact.  Delta: N arrays (p, c)."""
+    N = len(Delta)
+    p, c = Delta[0].shape
+    L = c + N - 2
+    x = [f32(Delta[i][:, 0]) for i in range(N)]
+    Y = [[None] * (L + 1) for _ in range(N)]
+    for k in range(1, L + 1):
+        recv = [x[(i - 1) % N] for i in range(N)]
+        nxt = []
+        for i in range(N):
+            if k <= N - 1:
+                Y[i][k - 1] = recv[i]
+                v = f32(recv[i] + Delta[i][:, k])
+            else:
+                j = k - N + 1
+                Y[i][N - 2 + j] = recv[i]
+                if k + 1 <= c:
+                    v = recv[i] - Delta[i][:, j - 1] + Delta[i][:, k]
+                    v = f32(v) if one_rounding else f32(f32(recv[i] - Delta[i][:, j - 1]) + Delta[i][:, k])
+                else:
+                    v = f32(recv[i] - Delta[i][:, j - 1])
+            nxt.append(v)
+        x = nxt
+    for i in range(N):
+        Y[i][L] = Delta[i][:, c - 1]           # D_{i,c} keeps delta_{i,c}
+    return [np.column_stack(Y[i]) for i in range(N)]
+
+
+def fp32_protocol_floor(g, U, R):
+    """Relative l2 error, against the fp64 oracle, of the protocol itself run
+    with fp32 coefficients, fp32-stored encoded chunks and fp32 messages
+    (one rounding per round), encode and decode otherwise exact: what any
+    implementation with fp32 messages carries.  g: (N, d) host gradients."""
+    N = g.shape[0]
+    c = U.shape[1]
+    G = [oracle_chunks(g[i], c) for i in range(N)]
+    ref = OR.allreduce_chunks(G, U, R)
+    Uf, Rf = f32(U), f32(R)
+    Y = fp32_observations([f32(G[i] @ Uf[i]) for i in range(N)], True)
+    return max(np.linalg.norm(Y[i] @ Rf[i] - ref[i]) / np.linalg.norm(ref[i]) for i in range(N))

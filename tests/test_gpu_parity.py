@@ -604,6 +604,48 @@ def test_bucketed_batched_encode_and_decode(N, c, nb, kind):
         assert max_rel_l2(gpu[:, off:off + ln], ref) <= gate(kappa), (off, ln)
 
 
+def test_c128_at_the_top_of_the_kappa_range_stays_at_the_fp32_message_floor():
+    """N = 4, c = 128 on a kappa_max = 1e3 design (kappa_2(M) ~ 850), through
+    the single call (split-operand interior kernels and the tail) and the
+    bucketed call (batched fp32 kernels).  Here the protocol with fp32
+    messages is itself above 1e-4 (about 2.1 kappa u), so the bar is that
+    floor, computed on the host for the same plan and inputs: the kernels may
+    add at most 15 % to it (they round each message once, as the floor
+    does, and accumulate the contractions in fp32)."""
+    torch, dev = torch_dev()
+    from gpu_util import fp32_protocol_floor
+    N, c = 4, 128
+    U, R = case_plan(N, c, "kappa", 1e3)
+    kappa = OP.max_kappa_M(U)
+    plan = C.Plan.explicit(U, R)
+    d = 128 * 640 - 37
+    g = host_grads(N, d, seed=41)
+    work, ws, out = buffers(plan, d)
+    C.ring_simulate(plan, d, to_device(g), work, ws, out)
+    sync()
+    gpu = out.double().cpu().numpy()
+    parity = max_rel_l2(gpu, oracle_allreduce(g, U, R))
+    floor = fp32_protocol_floor(g, U, R)
+    print(f"N4-c128 kappa_M={kappa:.4g}: parity {parity:.3g}, fp32-message floor {floor:.3g}")
+    assert parity <= max(gate(kappa), 1.15 * floor)
+    rng = np.random.default_rng(43)
+    buckets = _bucket_list(rng, 4, c)
+    db = buckets[-1][0] + buckets[-1][1]
+    gb = host_grads(N, db, seed=44)
+    work_floats, ws_bytes = plan.bucketed_sizes([b[1] for b in buckets])
+    bwork = torch.empty((N, work_floats), dtype=torch.float32, device=dev)
+    bws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    bout = torch.full((N, db), float("nan"), dtype=torch.float32, device=dev)
+    C.ring_simulate_bucketed(plan, buckets, to_device(gb), bwork, bws, bout)
+    sync()
+    bgpu = bout.double().cpu().numpy()
+    for off, ln in buckets:
+        part = gb[:, off:off + ln]
+        par = max_rel_l2(bgpu[:, off:off + ln], oracle_allreduce(part, U, R))
+        fl = fp32_protocol_floor(part, U, R)
+        assert par <= max(gate(kappa), 1.15 * fl), (off, ln, par, fl)
+
+
 def test_copy_kernel():
     torch, dev = torch_dev()
     for n in (1, 7, 4096, 1_000_003):
