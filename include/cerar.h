@@ -31,8 +31,14 @@
  *    be recorded into a HIP graph by stream capture.  Work enqueued by calls
  *    that share buffers must be ordered by the caller (one stream does
  *    that).
- *  - All floating point on the device is IEEE fp32; plan construction is
- *    host fp64.
+ *  - Data on the device (gradients, encoded chunks, messages, outputs) is
+ *    IEEE fp32.  The encode and decode contractions accumulate in fp32; at
+ *    c = 128 their fp32 operands are split exactly into three bf16 terms and
+ *    six of the nine term products are summed on the bf16 matrix cores
+ *    (within two units of fp32 rounding per product).  A round forms
+ *    recv - delta_j + delta_{k+1} in fp64 and rounds the message to fp32
+ *    once.  The error norms accumulate in fp64.  Plan construction is host
+ *    fp64.
  */
 #ifndef CERAR_H
 #define CERAR_H
