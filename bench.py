@@ -352,7 +352,7 @@ def _oracle_worker(name, pos, U, R, seconds, keep, barrier, queue):
 def cpu_baseline(name, U, R, plan_desc, positions, seconds):
     """Time the fp64 oracle on the GPU line's own plan (U, R from the
     library's plan) over sampled positions of the same workload: one worker
-    process per host core of the machine's CPU share, each single-threaded on its
+    process per host core available to this process, each single-threaded on its
     own positions.  Runs before the process touches the GPU, so the workers
     are plain forks of a process with no device state."""
     import multiprocessing as mp
@@ -370,7 +370,7 @@ def cpu_baseline(name, U, R, plan_desc, positions, seconds):
         usable = len(os.sched_getaffinity(0))
     except AttributeError:
         usable = cores
-    # at most 15 workers: with the parent, within the 16 processes a one-GPU machine allows
+    # at most CPU_WORKERS_MAX workers, so that with the parent at most 16 processes run
     threads = max(1, min(usable, CPU_WORKERS_MAX))
     rng = np.random.default_rng(12345)
     per = max(1, min(positions, p // threads))
@@ -401,7 +401,7 @@ def cpu_baseline(name, U, R, plan_desc, positions, seconds):
             "extrapolated_step_s": round(step_bytes / (value * 1e9), 1),
             "plan": "the GPU line's plan (its fp64 U and R, from cerar_plan_get_matrices)",
             "sample": f"{len(pos_all)} sampled positions x {c} chunks x {N} workers of the same workload, split "
-                      f"over {threads} single-threaded processes (box: {cores} cores), each running the fp64 NumPy "
+                      f"over {threads} single-threaded processes (host: {cores} cores), each running the fp64 NumPy "
                       f"oracle (encode, Algorithm 1 lock-step, decode) on its positions repeatedly for "
                       f"{seconds:g} s ({done} positions in all); plan: {plan_desc}; GB/s counts the same "
                       f"algorithmic bytes per position as the GPU line"}
