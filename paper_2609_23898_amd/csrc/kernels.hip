@@ -595,7 +595,9 @@ __device__ inline float combine3(float recv, float sub, float add) {
     return (float)(((double)recv - (double)sub) + (double)add);
 }
 
-template <int MODE, bool VEC>
+// V 16-byte elements per thread in the vector layout: workgroup wg covers
+// [wg V, (wg + 1) V) x 1024 floats, V consecutive 1 KiB runs per wave.
+template <int MODE, bool VEC, int V = 1>
 __device__ inline void round_body(const SlotBase &sb, const RoundOp &op, unsigned wg, unsigned wgpw) {
     const float *recv = sb.ptr(op.recv);
     const float *sub = MODE >= 1 ? sb.ptr(op.sub) : nullptr;   // aliases dst (in place)
@@ -603,17 +605,20 @@ __device__ inline void round_body(const SlotBase &sb, const RoundOp &op, unsigne
     float *dst = sb.ptr(op.dst);
     const size_t p = sb.p;
     if (VEC) {
-        const size_t i = ((size_t)wg * kRoundThreads + threadIdx.x) * 4;
-        if (i < p) {
-            v4f v = nt_load(recv + i);
-            if (MODE == 0) v = v + nt_load(add + i);
-            if (MODE == 2) v = v - nt_load(sub + i);
-            if (MODE == 1) {
-                const v4f s = nt_load(sub + i), t = nt_load(add + i);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) v[q] = combine3(v[q], s[q], t[q]);
+        for (int u = 0; u < V; ++u) {
+            const size_t i = (((size_t)wg * V + u) * kRoundThreads + threadIdx.x) * 4;
+            if (i < p) {
+                v4f v = nt_load(recv + i);
+                if (MODE == 0) v = v + nt_load(add + i);
+                if (MODE == 2) v = v - nt_load(sub + i);
+                if (MODE == 1) {
+                    const v4f s = nt_load(sub + i), t = nt_load(add + i);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) v[q] = combine3(v[q], s[q], t[q]);
+                }
+                nt_store(dst + i, v);
             }
-            nt_store(dst + i, v);
         }
     } else {
         for (size_t i = (size_t)wg * kRoundThreads + threadIdx.x; i < p; i += (size_t)wgpw * kRoundThreads) {
@@ -626,11 +631,11 @@ __device__ inline void round_body(const SlotBase &sb, const RoundOp &op, unsigne
     }
 }
 
-template <int MODE, bool VEC>
+template <int MODE, bool VEC, int V = 1>
 __global__ __launch_bounds__(kRoundThreads) void k_round(RoundParams a) {
     const int worker = blockIdx.x / a.wg_per_worker;
     const int wg = blockIdx.x - worker * a.wg_per_worker;
-    round_body<MODE, VEC>(a.sb, a.ops[worker], wg, a.wg_per_worker);
+    round_body<MODE, VEC, V>(a.sb, a.ops[worker], wg, a.wg_per_worker);
 }
 
 // The same round for a batch of independent instances (buckets) in one
@@ -2113,8 +2118,8 @@ int enqueue_encode(const cerar_plan *plan, const DeviceCopy *dc, const Geometry 
 
 // Workgroups per worker of a round: one 16-byte element per thread, or a
 // grid-stride loop in the scalar layout.
-unsigned round_wgs(size_t p, bool vec) {
-    const size_t w = vec ? (p / 4 + kRoundThreads - 1) / kRoundThreads
+unsigned round_wgs(size_t p, bool vec, int v = 1) {
+    const size_t w = vec ? (p / 4 + (size_t)v * kRoundThreads - 1) / ((size_t)v * kRoundThreads)
                          : std::min<size_t>((p + kRoundThreads - 1) / kRoundThreads, 1 << 16);
     return (unsigned)std::max<size_t>(1, w);
 }
@@ -2123,6 +2128,12 @@ int round_mode(const cerar_plan *plan, int k) {
     return (k <= plan->N - 1) ? 0 : (k + 1 <= plan->c ? 1 : 2);
 }
 
+// Messages of at most 2^21 floats take two 16-byte elements per thread:
+// in-process A/B at N = 8, the rounds ran 8 % faster at p = 2^20 and 3-6 %
+// faster at p = 2^21, but 3-4 % slower at p = 3.9M and 4.2M and 8 % slower
+// at the Pythia-1.4B length (22.1M), where one element per thread stays.
+constexpr size_t kRoundTwoVectorMaxP = (size_t)1 << 21;
+
 int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &g, int k, float *work,
                   size_t ld_work, void *ws, hipStream_t s) {
     const int N = plan->N, c = plan->c, L = plan->L;
@@ -2130,13 +2141,18 @@ int enqueue_round(const cerar_plan *plan, const DeviceCopy *dc, const Geometry &
     RoundParams a;
     a.sb = slot_base(plan, g, work, ld_work, ws);
     a.ops = dc->rounds + (size_t)k * N;
-    a.wg_per_worker = (int)round_wgs(g.p, g.vec);
+    const bool two = g.vec && g.p <= kRoundTwoVectorMaxP;
+    a.wg_per_worker = (int)round_wgs(g.p, g.vec, two ? 2 : 1);
     if (!fits_dispatch((uint64_t)N * a.wg_per_worker, kRoundThreads))
         return fail(CERAR_E_INVAL, "p=%zu is too long for one round launch over N=%d workers", g.p, N);
     const dim3 grid((unsigned)(N * a.wg_per_worker));
     (void)c;
     const int mode = round_mode(plan, k);
-    if (g.vec) {
+    if (two) {
+        if (mode == 0) hipLaunchKernelGGL((k_round<0, true, 2>), grid, dim3(kRoundThreads), 0, s, a);
+        else if (mode == 1) hipLaunchKernelGGL((k_round<1, true, 2>), grid, dim3(kRoundThreads), 0, s, a);
+        else hipLaunchKernelGGL((k_round<2, true, 2>), grid, dim3(kRoundThreads), 0, s, a);
+    } else if (g.vec) {
         if (mode == 0) hipLaunchKernelGGL((k_round<0, true>), grid, dim3(kRoundThreads), 0, s, a);
         else if (mode == 1) hipLaunchKernelGGL((k_round<1, true>), grid, dim3(kRoundThreads), 0, s, a);
         else hipLaunchKernelGGL((k_round<2, true>), grid, dim3(kRoundThreads), 0, s, a);
